@@ -1,0 +1,180 @@
+"""Benchmark: MeqMuon steps/s over all hidden 2D weights of the 1B shape on one MI355X.
+
+One step = one meq_step over all 112 hidden matrices of the 1B-shape Llama
+(16 layers, d 2048, ffn 8192, GQA 32/8 heads of dim 64): momentum, Newton-Schulz
+(5 steps, bf16 MFMA), row/column equilibration and the write-back, bf16 weights
+and gradients, fp32 momentum, inputs resident in HBM.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "MeqMuon steps/sec over all hidden 2D weights (1B shape); NS MFMA %, norm GB/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def ns_flops(s: int, l: int, steps: int):
+    """Algorithmic Newton-Schulz flops of one matrix: (symmetric-aware total, apply-only, dense total)."""
+    sym = steps * (3 * s * s * l + s ** 3)
+    apply = steps * (2 * s * s * l)
+    dense = steps * (4 * s * s * l + 2 * s ** 3)
+    return sym, apply, dense
+
+
+def stage_bytes(elems: int, param_bytes: int):
+    """Algorithmic HBM bytes per element of the byte stages: momentum (G, B read+write, bf16 V),
+    row/column sums (U), write-back (U, W read+write)."""
+    return {"momentum": elems * (param_bytes + 4 + 4 + 2), "rowcol": elems * 2,
+            "update": elems * (2 + 2 * param_bytes)}
+
+
+def cpu_baseline_leg(wl, lr: float, budget_s: float):
+    """Time the fp64 oracle on one matrix of each distinct shape and scale to a whole step."""
+    import numpy as np
+
+    import oracle
+    import workloads
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([int(i.get("num_threads", 1)) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        threads = len(os.sched_getaffinity(0))
+    hp = oracle.HParams()
+    first = {}
+    for i, m in enumerate(wl.matrices):
+        first.setdefault((m.rows, m.cols), []).append(i)
+    per_shape = {}
+    spent = 0.0
+    for shape, idxs in sorted(first.items(), key=lambda kv: kv[0][0] * kv[0][1]):
+        i = idxs[0]
+        w0 = workloads.weight_init(wl, i).astype(np.float64)
+        g = workloads.grad_at_step(wl, i, 0).astype(np.float64)
+        t0 = time.perf_counter()
+        oracle.meq_step(w0, g, np.zeros_like(w0), hp, lr, wide=True)
+        dt = time.perf_counter() - t0
+        per_shape[shape] = (dt, len(idxs))
+        spent += dt
+        if spent > budget_s:
+            break
+    if len(per_shape) < len(first):
+        return None
+    sec_per_step = sum(dt * n for dt, n in per_shape.values())
+    sample = ", ".join(f"{r}x{c}: {dt:.2f} s x {n}" for (r, c), (dt, n) in per_shape.items())
+    return {"value": 1.0 / sec_per_step, "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp64 numpy oracle, one matrix of each shape timed once (wide-orientation NS), "
+                      f"scaled by shape counts to the full {wl.count}-matrix step: {sample}; "
+                      f"est. {sec_per_step:.1f} s/step"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama-1b")
+    ap.add_argument("--lr", type=float, default=0.02)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=30.0, help="seconds of oracle work at most")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the MeqMuon update is measured on a single MI355X; "
+              f"--gpus {args.gpus} is not supported (multi-GPU sharding is a design note, not built)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    import workloads
+    from paper_2609_35701_amd import meq
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda:0")
+    wl = workloads.workload(args.workload)
+    print(f"# bench: workload {wl.name}, {wl.count} matrices, {wl.elements} elements", file=sys.stderr, flush=True)
+    params, grads, _ = workloads.device_inputs(wl, dev)
+    upd = meq.HiddenWeightUpdate(params)
+    hp = upd.plan.hparams
+    print(f"# bench: workspace {upd.plan.workspace_bytes / 2**30:.2f} GiB, groups {upd.plan.groups()}",
+          file=sys.stderr, flush=True)
+    stream = torch.cuda.current_stream(dev)
+    for _ in range(args.warmup):
+        upd.step(grads, args.lr)
+    torch.cuda.synchronize()
+    # timed region: per-kernel HIP events on the launch stream for every kernel kind
+    upd.plan.set_timing(range(len(meq.KERNEL_NAMES)))
+    for k in range(len(meq.KERNEL_NAMES)):
+        upd.plan.get_timing(k, reset=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        upd.step(grads, args.lr)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    upd.plan.set_timing([])
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    kern = {}
+    for k, name in enumerate(meq.KERNEL_NAMES):
+        ms, n = upd.plan.get_timing(k)
+        kern[name] = {"ms_per_step": ms / args.steps, "launches_per_step": n / args.steps,
+                      "avg_launch_ms": ms / n if n else None}
+    print(f"# bench: {ms_per_step:.3f} ms/step; " +
+          ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in kern.items()), file=sys.stderr, flush=True)
+
+    sym = apply = dense = 0
+    for m in wl.matrices:
+        s, l = min(m.rows, m.cols), max(m.rows, m.cols)
+        a, b, c = ns_flops(s, l, hp.ns_steps)
+        sym, apply, dense = sym + a, apply + b, dense + c
+    pbytes = 2 if wl.param_dtype == "bf16" else 4
+    sb = stage_bytes(wl.elements, pbytes)
+    ns_ms = sum(kern[k]["ms_per_step"] for k in ("gram", "poly", "apply"))
+    ap_ms = kern["apply"]["ms_per_step"]
+    apply_tflops = apply / (ap_ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "kernel": "k_ns_gemm<2> (X <- aX + P X, bf16 MFMA)",
+                "achieved": apply_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": apply_tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                "flops_per_launch": apply / max(kern["apply"]["launches_per_step"], 1),
+                "avg_launch_ms": kern["apply"]["avg_launch_ms"]}
+    stages = {
+        "ns_tflops_sym": sym / (ns_ms * 1e-3) / 1e12,
+        "ns_frac_of_peak_sym": sym / (ns_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "ns_tflops_dense": dense / (ns_ms * 1e-3) / 1e12,
+        "momentum_gbs": sb["momentum"] / (kern["momentum"]["ms_per_step"] * 1e-3) / 1e9,
+        "rowcol_gbs": sb["rowcol"] / (kern["rowcol"]["ms_per_step"] * 1e-3) / 1e9,
+        "update_gbs": sb["update"] / (kern["update"]["ms_per_step"] * 1e-3) / 1e9,
+        "byte_stages_gbs": sum(sb.values()) / (sum(kern[k]["ms_per_step"] for k in ("momentum", "rowcol", "update"))
+                                               * 1e-3) / 1e9,
+    }
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("# bench: timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
+        cpu = cpu_baseline_leg(wl, args.lr, args.cpu_budget)
+    line = {
+        "metric": METRIC, "value": 1e3 / ms_per_step, "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "matrices": wl.count, "elements": wl.elements,
+                   "param_dtype": wl.param_dtype, "grad_dtype": wl.param_dtype, "momentum_dtype": "f32",
+                   "ns_steps": hp.ns_steps, "ns_tflop_per_step_sym": sym / 1e12,
+                   "ns_tflop_per_step_dense": dense / 1e12},
+        "roofline": roofline, "cpu_baseline": cpu, "stages": stages,
+        "kernels_ms_per_step": {k: v["ms_per_step"] for k, v in kern.items()},
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

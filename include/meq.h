@@ -1,0 +1,205 @@
+/*
+ * meq.h - C ABI of the MeqMuon hidden-weight update for AMD MI355X (gfx950).
+ *
+ * One call of meq_step performs, for every 2D hidden-layer weight W (m x n,
+ * row-major, rows = output features), the hidden-weight branch of the paper's
+ * Algorithm "MeqMuon" (arxiv 2609.35701, Section "MeqMuon"):
+ *
+ *   B   <- mu * B + G                                   eq. "momentum"
+ *   V   <- B            (or G + mu * B when nesterov)   Section "Experiments"
+ *   U   <- K quintic Newton-Schulz steps on V / ||V||_F eq. "ns"
+ *   r,c <- row / column RMS of U                        eq. "row-col-rms"
+ *   U~  <- N_r(U) if CV(r) >= CV(c) else N_c(U)         eqs. "cv", "operators", "hidden"
+ *   W   <- (1 - lr * lambda) * W - rho * lr * U~        eq. "meqmuon-update"
+ *
+ * Conventions shared by every entry point
+ *   - Matrices are dense, contiguous, row-major; element (i, j) of an m x n
+ *     matrix sits at offset i * n + j.
+ *   - "Device pointer" means memory allocated on the HIP device the stream
+ *     belongs to (hipMalloc or a torch CUDA/HIP tensor).  The library never
+ *     allocates, frees or takes ownership of caller memory.
+ *   - Functions that return meq_status validate every argument before any
+ *     device work; on an argument error nothing is enqueued and no caller
+ *     memory is modified.  HIP failures are reported as MEQ_ERR_HIP.
+ *   - No entry point blocks the host except meq_get_stats and
+ *     meq_get_timing, which synchronize with the given stream.
+ *   - A plan is not reentrant: do not run two meq_step calls of one plan (or
+ *     two plans sharing one workspace) concurrently on different streams.
+ */
+#ifndef MEQ_H
+#define MEQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MEQ_OK = 0,
+  MEQ_ERR_INVALID_ARG = -1, /* a null pointer, a bad size or hyperparameter, a count mismatch   */
+  MEQ_ERR_UNSUPPORTED = -2, /* a dtype combination or size the library does not implement        */
+  MEQ_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed                          */
+  MEQ_ERR_WORKSPACE = -4    /* the workspace is null, too small or not 256-byte aligned           */
+} meq_status;
+
+typedef enum { MEQ_F32 = 0, MEQ_BF16 = 1 } meq_dtype;
+
+/* Normalization direction chosen for a matrix (eq. "hidden"). */
+typedef enum { MEQ_DIR_ROW = 0, MEQ_DIR_COL = 1 } meq_direction;
+
+/*
+ * Hyperparameters of the update (Section "Experiments"; delta from Section
+ * "Imbalance patterns").  The learning rate eta_t is passed to each meq_step.
+ *   mu             momentum coefficient, 0 <= mu < 1
+ *   rho            RMS alignment coefficient, rho > 0
+ *   weight_decay   decoupled weight decay lambda >= 0
+ *   ns_steps       number K of Newton-Schulz steps, 1 <= K <= 64
+ *   ns_a/b/c       quintic coefficients (a, b, c), finite
+ *   zero_rms_delta RMS values at or below delta count as zero, delta >= 0
+ *   nesterov       0: orthogonalize B_t (Algorithm "MeqMuon");
+ *                  1: orthogonalize G_t + mu * B_t
+ */
+typedef struct {
+  float mu;
+  float rho;
+  float weight_decay;
+  int32_t ns_steps;
+  float ns_a;
+  float ns_b;
+  float ns_c;
+  float zero_rms_delta;
+  int32_t nesterov;
+} meq_hparams;
+
+/*
+ * One hidden-layer weight: rows x cols, with its parameter and gradient dtype.
+ * Supported (param, grad) pairs: (MEQ_F32, MEQ_F32) and (MEQ_BF16, MEQ_BF16).
+ * The momentum is always float32 with the same shape (one value per element,
+ * the paper's optimizer-state accounting in Table "experiment-efficiency").
+ * 1 <= rows, cols <= 65536.
+ */
+typedef struct {
+  int64_t rows;
+  int64_t cols;
+  int32_t param_dtype; /* meq_dtype */
+  int32_t grad_dtype;  /* meq_dtype */
+} meq_matrix_desc;
+
+typedef struct meq_plan meq_plan; /* opaque; owns host metadata only */
+
+/* Fill *hp with the paper's defaults: mu 0.95, rho 0.2, lambda 0.1, K 5,
+ * (a, b, c) = (3.4445, -4.7750, 2.0315), delta 1e-7, nesterov 0.  No-op on null. */
+void meq_default_hparams(meq_hparams* hp);
+
+/*
+ * Validate `count` matrix descriptors and the hyperparameters and build a plan:
+ * the matrices are grouped by shape for batched Newton-Schulz launches and the
+ * workspace layout is fixed.  Touches no device and may run without a GPU.
+ * count == 0 is allowed (meq_step is then a no-op).  On success *out receives a
+ * plan the caller releases with meq_destroy; on failure *out is set to NULL.
+ */
+meq_status meq_init(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out);
+
+/* Bytes of device workspace meq_step needs for this plan (0 for a null plan). */
+size_t meq_workspace_bytes(const meq_plan* plan);
+
+/*
+ * Enqueue one update of every matrix of the plan on `stream` (0 = the null
+ * stream of the current device).
+ *   params[i]   device pointer, rows x cols of param_dtype; updated in place
+ *   grads[i]    device pointer, rows x cols of grad_dtype; read only
+ *   momenta[i]  device pointer, rows x cols float32; updated in place; zero
+ *               before the first step (B_{-1} = 0)
+ *   lr          learning rate eta_t of this step (finite, >= 0)
+ *   workspace   device pointer, 256-byte aligned, at least workspace_bytes bytes,
+ *               >= meq_workspace_bytes(plan); its contents need not be preserved
+ *               between calls, but it must not be used by anything else while
+ *               the step runs.  It also holds the statistics read by
+ *               meq_get_stats until the next meq_step.
+ * The three pointer arrays are host arrays of `count` entries (count as given to
+ * meq_init) and are only read during the call.  Parameters, gradients and
+ * momenta of different matrices must not overlap each other or the workspace.
+ * Returns after enqueuing; the update is complete when the stream reaches it.
+ */
+meq_status meq_step(meq_plan* plan, void* const* params, const void* const* grads, float* const* momenta,
+                    float lr, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Copy the last step's per-matrix statistics from the workspace to host arrays
+ * of `count` entries (any of them may be null): gamma_r, gamma_c are the row
+ * and column CVs of U (eq. "cv", computed in double precision), dir the chosen
+ * meq_direction.  Synchronizes with `stream`.
+ */
+meq_status meq_get_stats(const meq_plan* plan, const void* workspace, double* gamma_r, double* gamma_c,
+                         int32_t* dir, hipStream_t stream);
+
+/* Release a plan (null is a no-op).  Pending timing events are destroyed. */
+void meq_destroy(meq_plan* plan);
+
+/* A static, human-readable description of a status code. */
+const char* meq_status_string(meq_status s);
+
+/* ----------------------------------------------------------------------------
+ * Introspection (host only, no device work)
+ * ------------------------------------------------------------------------- */
+
+/* Number of Newton-Schulz shape groups (matrices with equal (min, max) dims). */
+int32_t meq_plan_num_groups(const meq_plan* plan);
+
+/* Shape group g: short side s, long side l (after transposing tall matrices to
+ * wide orientation) and its number of matrices. */
+meq_status meq_plan_group(const meq_plan* plan, int32_t g, int64_t* s, int64_t* l, int32_t* count);
+
+/* Buffers of the workspace that tests may inspect after a step. */
+typedef enum {
+  MEQ_BUF_X0 = 0,      /* bf16 V (not yet divided by ||V||_F), wide orientation s x l, ld = padded l  */
+  MEQ_BUF_U = 1,       /* bf16 Newton-Schulz output U, wide orientation s x l, ld = padded l          */
+  MEQ_BUF_NORMSQ = 2,  /* double ||V||_F^2, 1 x 1                                                    */
+  MEQ_BUF_ROW_RMS = 3, /* double r of U in the matrix's own orientation, 1 x rows                      */
+  MEQ_BUF_COL_RMS = 4, /* double c of U in the matrix's own orientation, 1 x cols                      */
+  MEQ_BUF_SCALE = 5    /* float per-row (dir row, 1 x rows) or per-column (1 x cols) scale of U~ = U*s */
+} meq_buffer_kind;
+
+/*
+ * Locate buffer `kind` of matrix `matrix` inside the workspace: byte *offset from
+ * the workspace start, logical *rows x *cols and leading dimension *ld in elements.
+ * For MEQ_BUF_SCALE the extent depends on the direction chosen at run time; the
+ * region returned covers max(rows, cols) entries.  Any output may be null.
+ */
+meq_status meq_debug_region(const meq_plan* plan, int32_t matrix, int32_t kind, size_t* offset, int64_t* rows,
+                            int64_t* cols, int64_t* ld);
+
+/* ----------------------------------------------------------------------------
+ * Per-kernel timing with HIP events on the launch stream
+ * ------------------------------------------------------------------------- */
+
+typedef enum {
+  MEQ_K_MOMENTUM = 0, /* momentum + ||V||^2 partials + bf16 V in wide orientation            */
+  MEQ_K_NORM = 1,     /* ||V||_F^2 finalization                                                */
+  MEQ_K_GRAM = 2,     /* A = X X^T (symmetric tiles)                                           */
+  MEQ_K_POLY = 3,     /* P = b A + c A A (symmetric tiles)                                     */
+  MEQ_K_APPLY = 4,    /* X <- a X + P X                                                        */
+  MEQ_K_ROWCOL = 5,   /* row and column sums of squares of U                                    */
+  MEQ_K_SELECT = 6,   /* CVs, direction, scale vector                                           */
+  MEQ_K_UPDATE = 7,   /* decoupled weight decay + normalized update write-back                   */
+  MEQ_K_COUNT = 8
+} meq_kernel_kind;
+
+/* Bracket every launch of the kinds in `kind_mask` (bit k = meq_kernel_kind k)
+ * with HIP events on the launch stream from the next meq_step on; 0 turns timing off. */
+meq_status meq_set_timing(meq_plan* plan, uint32_t kind_mask);
+
+/* Synchronize the recorded events, add their durations to the plan's totals and
+ * report, for kernel kind `kind`, the accumulated milliseconds and launch count
+ * since the last reset (reset != 0 clears the totals after reading). */
+meq_status meq_get_timing(meq_plan* plan, int32_t kind, double* total_ms, int64_t* launches, int32_t reset);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEQ_H */

@@ -1,0 +1,388 @@
+// Streaming kernels of the MeqMuon hidden-weight update (HBM-bound stages):
+//   momentum + Frobenius partials + bf16 V in wide orientation   eq. "momentum", eq. "ns" (X_0)
+//   ||V||_F^2 finalization                                         eq. "ns" (X_0 = H / ||H||_F)
+//   row / column sums of squares of U                              eq. "row-col-rms"
+//   CVs, direction and scale vector                                 eqs. "cv", "operators", "hidden"
+//   decoupled weight decay + normalized update                      eq. "meqmuon-update"
+// All reductions are fixed-order trees (no floating-point atomics), so results
+// are bitwise reproducible run to run.
+#include "meq_internal.h"
+
+namespace meq {
+
+namespace {
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
+
+// float -> bfloat16, round to nearest, ties to even; NaN stays NaN (quieted).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Sum over a 256-thread block in a fixed order; every thread gets the result.
+template <typename T>
+__device__ __forceinline__ T block_sum256(T v, T* red /* >= 4 entries */) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  T r = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ int find_matrix(const int* tile_start, int count, int bid) {
+  int mi = 0;
+  while (mi + 1 < count && bid >= tile_start[mi + 1]) ++mi;
+  return mi;
+}
+
+// --------------------------------------------------------------------------------
+// Momentum B <- mu B + G, V = B (or G + mu B), per-tile sum of V^2, bf16 V written
+// into the zero-padded wide buffer (transposed through LDS for tall matrices).
+// One block = one 64 x 64 tile of the padded matrix in its own orientation;
+// thread (ty, tx) owns rows ty + 16 k (k < 4) and columns 4 tx .. 4 tx + 3.
+template <bool kGradBf16>
+__global__ __launch_bounds__(256) void k_momentum(MomentumArgs a) {
+  __shared__ uint16_t tr[kEwTile][kEwTile + 4];
+  __shared__ float red[4];
+  const int mi = find_matrix(a.tile_start, a.count, blockIdx.x);
+  const int t = blockIdx.x - a.tile_start[mi];
+  const int tcols = a.tiles_c[mi];
+  const int r0 = (t / tcols) * kEwTile, c0 = (t % tcols) * kEwTile;
+  const int m = a.m[mi], n = a.n[mi];
+  const bool tall = a.tall[mi] != 0;
+  const int64_t ldx = a.ldx[mi];
+  float* __restrict__ bp = a.b[mi];
+  uint16_t* __restrict__ xp = a.x[mi];
+  const float mu = a.mu;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const bool vec = (n & 3) == 0;
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int row = r0 + ty + 16 * k;
+    const int col = c0 + 4 * tx;
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (row < m && col < n) {
+      const int64_t off = static_cast<int64_t>(row) * n + col;
+      float g[4], b[4];
+      if (vec) {
+        float4 bv = *reinterpret_cast<const float4*>(bp + off);
+        b[0] = bv.x; b[1] = bv.y; b[2] = bv.z; b[3] = bv.w;
+        if (kGradBf16) {
+          uint2 gv = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.g[mi]) + off);
+          g[0] = bf16_to_f32(gv.x & 0xffffu); g[1] = bf16_to_f32(gv.x >> 16);
+          g[2] = bf16_to_f32(gv.y & 0xffffu); g[3] = bf16_to_f32(gv.y >> 16);
+        } else {
+          float4 gv = *reinterpret_cast<const float4*>(static_cast<const float*>(a.g[mi]) + off);
+          g[0] = gv.x; g[1] = gv.y; g[2] = gv.z; g[3] = gv.w;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          b[q] = fmaf(mu, b[q], g[q]);
+          v[q] = a.nesterov ? fmaf(mu, b[q], g[q]) : b[q];
+        }
+        *reinterpret_cast<float4*>(bp + off) = make_float4(b[0], b[1], b[2], b[3]);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (col + q < n) {
+            const float gq = kGradBf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.g[mi])[off + q])
+                                       : static_cast<const float*>(a.g[mi])[off + q];
+            const float bq = fmaf(mu, bp[off + q], gq);
+            bp[off + q] = bq;
+            v[q] = a.nesterov ? fmaf(mu, bq, gq) : bq;
+          }
+        }
+      }
+    }
+    uint16_t h[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      ss = fmaf(v[q], v[q], ss);
+      h[q] = f32_to_bf16(v[q]);
+    }
+    if (!tall) {
+      uint2 pk;
+      pk.x = h[0] | (static_cast<uint32_t>(h[1]) << 16);
+      pk.y = h[2] | (static_cast<uint32_t>(h[3]) << 16);
+      *reinterpret_cast<uint2*>(xp + static_cast<int64_t>(row) * ldx + col) = pk;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) tr[4 * tx + q][ty + 16 * k] = h[q];
+    }
+  }
+  if (tall) {
+    __syncthreads();
+    // wide row = own column, wide column = own row
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int wr = ty + 16 * k;  // local own-column index
+      const uint2 pk = *reinterpret_cast<const uint2*>(&tr[wr][4 * tx]);
+      *reinterpret_cast<uint2*>(xp + static_cast<int64_t>(c0 + wr) * ldx + r0 + 4 * tx) = pk;
+    }
+  }
+  const float tot = block_sum256(ss, red);
+  if (threadIdx.x == 0) a.part[mi][t] = tot;
+}
+
+// --------------------------------------------------------------------------------
+// ||V||_F^2 = sum of the tile partials (fixed order, in double), then 1/||V|| and
+// 1/||V||^2 for the Newton-Schulz prescale folded into the first iteration.
+__global__ __launch_bounds__(256) void k_norm(NormArgs a) {
+  __shared__ double red[4];
+  const int mi = blockIdx.x;
+  const float* p = a.part[mi];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < a.nparts[mi]; i += 256) s += static_cast<double>(p[i]);
+  s = block_sum256(s, red);
+  if (threadIdx.x == 0) {
+    MatScalars* sc = a.scal[mi];
+    sc->normsq = s;
+    sc->inv_norm = s > 0.0 ? static_cast<float>(1.0 / sqrt(s)) : 0.f;
+    sc->inv_normsq = s > 0.0 ? static_cast<float>(1.0 / s) : 0.f;
+    a.fold[mi][0] = sc->inv_norm;
+    a.fold[mi][1] = sc->inv_normsq;
+  }
+}
+
+// --------------------------------------------------------------------------------
+// Sums of squares of the bf16 U per row and per column of one 256 x 256 tile of
+// the wide buffer.  Thread t owns columns 8 (t % 32) .. +7 of rows t / 32 + 8 q.
+__global__ __launch_bounds__(256) void k_rowcol(RowColArgs a) {
+  __shared__ float csh[8][kTile];
+  const int mat = blockIdx.y;
+  const int ti = blockIdx.x / a.tiles_c, tj = blockIdx.x % a.tiles_c;
+  const uint16_t* __restrict__ u = a.u + mat * a.stride_u;
+  const int cg = threadIdx.x & 31, rg = threadIdx.x >> 5;
+  const int r0 = ti * kTile, c0 = tj * kTile;
+  float csum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  float* rp = a.rpart + mat * a.stride_rpart + static_cast<int64_t>(tj) * a.S + r0;
+  for (int q = 0; q < 32; ++q) {
+    const int r = rg + 8 * q;
+    const uint4 v = *reinterpret_cast<const uint4*>(u + static_cast<int64_t>(r0 + r) * a.L + c0 + 8 * cg);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    float rs = 0.f;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const float lo = bf16_to_f32(w[p] & 0xffffu), hi = bf16_to_f32(w[p] >> 16);
+      csum[2 * p] = fmaf(lo, lo, csum[2 * p]);
+      csum[2 * p + 1] = fmaf(hi, hi, csum[2 * p + 1]);
+      rs = fmaf(lo, lo, rs);
+      rs = fmaf(hi, hi, rs);
+    }
+#pragma unroll
+    for (int off = 16; off > 0; off >>= 1) rs += __shfl_xor(rs, off, 64);
+    if (cg == 0) rp[r] = rs;
+  }
+#pragma unroll
+  for (int p = 0; p < 8; ++p) csh[rg][8 * cg + p] = csum[p];
+  __syncthreads();
+  const int c = threadIdx.x;
+  float s = 0.f;
+#pragma unroll
+  for (int g = 0; g < 8; ++g) s += csh[g][c];
+  a.cpart[mat * a.stride_cpart + static_cast<int64_t>(ti) * a.L + c0 + c] = s;
+}
+
+// --------------------------------------------------------------------------------
+// One block per matrix: finish r and c (eq. "row-col-rms") from the tile partials,
+// their CVs over entries above delta (eq. "cv", double, two passes), the direction
+// (rows iff gamma_r >= gamma_c, eq. "hidden") and the scale vector of N_r or N_c
+// (eq. "operators"; entries at or below delta get scale 0).
+__device__ double cv_of(const double* v, int len, double delta, double* red) {
+  double s = 0.0, cnt = 0.0;
+  for (int i = threadIdx.x; i < len; i += 256) {
+    const double x = v[i];
+    if (x > delta) { s += x; cnt += 1.0; }
+  }
+  s = block_sum256(s, red);
+  cnt = block_sum256(cnt, red);
+  if (cnt == 0.0) return 0.0;
+  const double mean = s / cnt;
+  double q = 0.0;
+  for (int i = threadIdx.x; i < len; i += 256) {
+    const double x = v[i];
+    if (x > delta) q += (x - mean) * (x - mean);
+  }
+  q = block_sum256(q, red);
+  return sqrt(q / cnt) / mean;
+}
+
+__global__ __launch_bounds__(256) void k_select(SelectArgs a) {
+  __shared__ double red[4];
+  const int mi = blockIdx.x;
+  const int m = a.m[mi], n = a.n[mi], S = a.S[mi], L = a.L[mi];
+  const bool tall = a.tall[mi] != 0;
+  const float* rpart = a.rpart[mi];  // (L/256) x S : per wide row
+  const float* cpart = a.cpart[mi];  // (S/256) x L : per wide column
+  const int nct = L / kTile, nrt = S / kTile;
+  double* rr = a.rrms[mi];
+  double* cc = a.crms[mi];
+  // wide row sums
+  const int s_dim = tall ? n : m;
+  const int l_dim = tall ? m : n;
+  for (int i = threadIdx.x; i < s_dim; i += 256) {
+    double t = 0.0;
+    for (int k = 0; k < nct; ++k) t += static_cast<double>(rpart[static_cast<int64_t>(k) * S + i]);
+    // wide row i is own row i (wide) or own column i (tall); divide by the own-orientation length
+    if (!tall) rr[i] = sqrt(t / n); else cc[i] = sqrt(t / m);
+  }
+  for (int j = threadIdx.x; j < l_dim; j += 256) {
+    double t = 0.0;
+    for (int k = 0; k < nrt; ++k) t += static_cast<double>(cpart[static_cast<int64_t>(k) * L + j]);
+    if (!tall) cc[j] = sqrt(t / m); else rr[j] = sqrt(t / n);
+  }
+  __syncthreads();
+  __threadfence_block();
+  const double gr = cv_of(rr, m, a.delta, red);
+  const double gc = cv_of(cc, n, a.delta, red);
+  const int dir = gr >= gc ? 0 : 1;
+  float* sc = a.scale[mi];
+  const double* v = dir == 0 ? rr : cc;
+  const int len = dir == 0 ? m : n;
+  for (int i = threadIdx.x; i < len; i += 256) {
+    const double x = v[i];
+    sc[i] = x > a.delta ? static_cast<float>(1.0 / x) : 0.f;
+  }
+  if (threadIdx.x == 0) {
+    MatScalars* s = a.scal[mi];
+    s->gamma_r = gr;
+    s->gamma_c = gc;
+    s->dir = dir;
+  }
+}
+
+// --------------------------------------------------------------------------------
+// W <- decay * W - step * U * scale  over 64 x 64 tiles of the matrix's own
+// orientation; U is read from the wide buffer (through LDS for tall matrices).
+template <bool kParamBf16>
+__global__ __launch_bounds__(256) void k_update(UpdateArgs a) {
+  __shared__ uint16_t tr[kEwTile][kEwTile + 4];
+  const int mi = find_matrix(a.tile_start, a.count, blockIdx.x);
+  const int t = blockIdx.x - a.tile_start[mi];
+  const int tcols = a.tiles_c[mi];
+  const int r0 = (t / tcols) * kEwTile, c0 = (t % tcols) * kEwTile;
+  const int m = a.m[mi], n = a.n[mi];
+  const bool tall = a.tall[mi] != 0;
+  const int64_t ldu = a.ldu[mi];
+  const uint16_t* __restrict__ u = a.u[mi];
+  const float* __restrict__ scale = a.scale[mi];
+  const int dir = a.scal[mi]->dir;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  if (tall) {
+    // own tile rows r0.., cols c0.. = wide rows c0.., wide cols r0..  (wide buffer is padded: no bounds)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int wr = ty + 16 * k;
+      const uint2 pk = *reinterpret_cast<const uint2*>(u + static_cast<int64_t>(c0 + wr) * ldu + r0 + 4 * tx);
+      *reinterpret_cast<uint2*>(&tr[wr][4 * tx]) = pk;
+    }
+    __syncthreads();
+  }
+  const bool vec = (n & 3) == 0;
+  const float decay = a.decay, step = a.step;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int lr = ty + 16 * k;
+    const int row = r0 + lr;
+    const int col = c0 + 4 * tx;
+    if (row >= m || col >= n) continue;
+    float uu[4];
+    if (!tall) {
+      const uint2 pk = *reinterpret_cast<const uint2*>(u + static_cast<int64_t>(row) * ldu + col);
+      uu[0] = bf16_to_f32(pk.x & 0xffffu); uu[1] = bf16_to_f32(pk.x >> 16);
+      uu[2] = bf16_to_f32(pk.y & 0xffffu); uu[3] = bf16_to_f32(pk.y >> 16);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) uu[q] = bf16_to_f32(tr[4 * tx + q][lr]);
+    }
+    float s[4];
+    if (dir == 0) {
+      const float sr = scale[row];
+      s[0] = s[1] = s[2] = s[3] = sr;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s[q] = (col + q < n) ? scale[col + q] : 0.f;
+    }
+    const int64_t off = static_cast<int64_t>(row) * n + col;
+    if (kParamBf16) {
+      uint16_t* wp = static_cast<uint16_t*>(a.w[mi]);
+      if (vec) {
+        uint2 pk = *reinterpret_cast<const uint2*>(wp + off);
+        float w[4] = {bf16_to_f32(pk.x & 0xffffu), bf16_to_f32(pk.x >> 16), bf16_to_f32(pk.y & 0xffffu),
+                      bf16_to_f32(pk.y >> 16)};
+        uint16_t h[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) h[q] = f32_to_bf16(fmaf(decay, w[q], -step * (uu[q] * s[q])));
+        pk.x = h[0] | (static_cast<uint32_t>(h[1]) << 16);
+        pk.y = h[2] | (static_cast<uint32_t>(h[3]) << 16);
+        *reinterpret_cast<uint2*>(wp + off) = pk;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (col + q < n) wp[off + q] = f32_to_bf16(fmaf(decay, bf16_to_f32(wp[off + q]), -step * (uu[q] * s[q])));
+      }
+    } else {
+      float* wp = static_cast<float*>(a.w[mi]);
+      if (vec) {
+        float4 wv = *reinterpret_cast<const float4*>(wp + off);
+        wv.x = fmaf(decay, wv.x, -step * (uu[0] * s[0]));
+        wv.y = fmaf(decay, wv.y, -step * (uu[1] * s[1]));
+        wv.z = fmaf(decay, wv.z, -step * (uu[2] * s[2]));
+        wv.w = fmaf(decay, wv.w, -step * (uu[3] * s[3]));
+        *reinterpret_cast<float4*>(wp + off) = wv;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (col + q < n) wp[off + q] = fmaf(decay, wp[off + q], -step * (uu[q] * s[q]));
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_momentum(const MomentumArgs& a, int grad_bf16, int total_tiles, hipStream_t st) {
+  if (grad_bf16)
+    hipLaunchKernelGGL(k_momentum<true>, dim3(total_tiles), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(k_momentum<false>, dim3(total_tiles), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm(const NormArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_norm, dim3(a.count), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rowcol(const RowColArgs& a, int batch, hipStream_t st) {
+  hipLaunchKernelGGL(k_rowcol, dim3(a.tiles_r * a.tiles_c, batch), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(const SelectArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_select, dim3(a.count), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_update(const UpdateArgs& a, int param_bf16, int total_tiles, hipStream_t st) {
+  if (param_bf16)
+    hipLaunchKernelGGL(k_update<true>, dim3(total_tiles), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(k_update<false>, dim3(total_tiles), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace meq

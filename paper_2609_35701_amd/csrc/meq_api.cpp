@@ -1,0 +1,538 @@
+// Host side of the MeqMuon C ABI: argument validation, shape grouping, the
+// workspace layout, and the launch sequence of one step (Algorithm "MeqMuon",
+// hidden-weight branch).  meq_init touches no device; meq_step only enqueues.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <new>
+#include <utility>
+#include <vector>
+
+#include "meq.h"
+#include "meq_internal.h"
+
+#define MEQ_EXPORT extern "C" __attribute__((visibility("default")))
+
+using namespace meq;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kMaxDim = 65536;
+// Every per-matrix wide buffer must stay addressable with 32-bit byte offsets.
+constexpr int64_t kMaxWideBytes = (int64_t{1} << 31) - 1;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+struct MatInfo {
+  int64_t m, n, s, l, S, L;
+  bool tall;
+  int dtype;  // param dtype == grad dtype
+  int group, gidx;
+  int tiles_pad_r, tiles_pad_c;  // 64x64 tiles over the padded matrix in its own orientation
+  int tiles_upd_r, tiles_upd_c;  // 64x64 tiles over the real matrix
+  size_t off_part, off_rrms, off_crms, off_scale;
+};
+
+struct GroupInfo {
+  int64_t s, l, S, L;
+  std::vector<int> mats;
+  size_t off_xa, off_xb, off_a, off_p, off_rpart, off_cpart, off_fold;
+  int64_t stride_x, stride_a, stride_rpart, stride_cpart;  // elements per matrix
+};
+
+struct TimedLaunch {
+  int kind;
+  hipEvent_t start, stop;
+};
+
+}  // namespace
+
+struct meq_plan {
+  meq_hparams hp;
+  std::vector<MatInfo> mats;
+  std::vector<GroupInfo> groups;
+  size_t off_scal = 0;
+  size_t ws_bytes = 0;
+  uint32_t timing_mask = 0;
+  std::vector<TimedLaunch> pending;
+  std::vector<hipEvent_t> event_pool;
+  double total_ms[MEQ_K_COUNT] = {};
+  int64_t launches[MEQ_K_COUNT] = {};
+};
+
+namespace {
+
+bool finite(float v) { return std::isfinite(v); }
+
+meq_status validate_hparams(const meq_hparams& hp) {
+  if (!finite(hp.mu) || hp.mu < 0.f || hp.mu >= 1.f) return MEQ_ERR_INVALID_ARG;
+  if (!finite(hp.rho) || hp.rho <= 0.f) return MEQ_ERR_INVALID_ARG;
+  if (!finite(hp.weight_decay) || hp.weight_decay < 0.f) return MEQ_ERR_INVALID_ARG;
+  if (hp.ns_steps < 1 || hp.ns_steps > 64) return MEQ_ERR_INVALID_ARG;
+  if (!finite(hp.ns_a) || !finite(hp.ns_b) || !finite(hp.ns_c)) return MEQ_ERR_INVALID_ARG;
+  if (!finite(hp.zero_rms_delta) || hp.zero_rms_delta < 0.f) return MEQ_ERR_INVALID_ARG;
+  if (hp.nesterov != 0 && hp.nesterov != 1) return MEQ_ERR_INVALID_ARG;
+  return MEQ_OK;
+}
+
+hipEvent_t take_event(meq_plan* p) {
+  if (!p->event_pool.empty()) {
+    hipEvent_t e = p->event_pool.back();
+    p->event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Launch `fn` (which returns the launch's hipError_t), bracketed by events when
+// the kind is being timed.
+template <typename F>
+meq_status timed_launch(meq_plan* p, int kind, hipStream_t st, F&& fn) {
+  const bool timed = (p->timing_mask >> kind) & 1u;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (timed) {
+    e0 = take_event(p);
+    e1 = take_event(p);
+    if (!e0 || !e1 || hipEventRecord(e0, st) != hipSuccess) return MEQ_ERR_HIP;
+  }
+  if (fn() != hipSuccess) return MEQ_ERR_HIP;
+  if (timed) {
+    if (hipEventRecord(e1, st) != hipSuccess) return MEQ_ERR_HIP;
+    p->pending.push_back({kind, e0, e1});
+  }
+  return MEQ_OK;
+}
+
+#define MEQ_TRY(expr)                 \
+  do {                                \
+    const meq_status _s = (expr);     \
+    if (_s != MEQ_OK) return _s;      \
+  } while (0)
+
+}  // namespace
+
+// ======================================================================== ABI
+MEQ_EXPORT void meq_default_hparams(meq_hparams* hp) {
+  if (!hp) return;
+  hp->mu = 0.95f;
+  hp->rho = 0.2f;
+  hp->weight_decay = 0.1f;
+  hp->ns_steps = 5;
+  hp->ns_a = 3.4445f;
+  hp->ns_b = -4.7750f;
+  hp->ns_c = 2.0315f;
+  hp->zero_rms_delta = 1e-7f;
+  hp->nesterov = 0;
+}
+
+MEQ_EXPORT const char* meq_status_string(meq_status s) {
+  switch (s) {
+    case MEQ_OK: return "ok";
+    case MEQ_ERR_INVALID_ARG: return "invalid argument";
+    case MEQ_ERR_UNSUPPORTED: return "unsupported dtype or size";
+    case MEQ_ERR_HIP: return "HIP runtime error";
+    case MEQ_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+  }
+  return "unknown status";
+}
+
+MEQ_EXPORT meq_status meq_init(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out) {
+  if (out) *out = nullptr;
+  if (!out || !hp || count < 0 || (count > 0 && !mats)) return MEQ_ERR_INVALID_ARG;
+  MEQ_TRY(validate_hparams(*hp));
+  for (int i = 0; i < count; ++i) {
+    const meq_matrix_desc& d = mats[i];
+    if (d.rows < 1 || d.cols < 1 || d.rows > kMaxDim || d.cols > kMaxDim) return MEQ_ERR_INVALID_ARG;
+    const bool known = (d.param_dtype == MEQ_F32 || d.param_dtype == MEQ_BF16) &&
+                       (d.grad_dtype == MEQ_F32 || d.grad_dtype == MEQ_BF16);
+    if (!known) return MEQ_ERR_INVALID_ARG;
+    if (d.param_dtype != d.grad_dtype) return MEQ_ERR_UNSUPPORTED;
+    const int64_t S = round_up(std::min(d.rows, d.cols), kTile), L = round_up(std::max(d.rows, d.cols), kTile);
+    if (S * L * 2 > kMaxWideBytes) return MEQ_ERR_UNSUPPORTED;
+  }
+  meq_plan* p = new (std::nothrow) meq_plan();
+  if (!p) return MEQ_ERR_INVALID_ARG;
+  p->hp = *hp;
+  p->mats.resize(count);
+  std::map<std::pair<int64_t, int64_t>, int> group_of;
+  for (int i = 0; i < count; ++i) {
+    MatInfo& mi = p->mats[i];
+    mi.m = mats[i].rows;
+    mi.n = mats[i].cols;
+    mi.tall = mi.m > mi.n;
+    mi.s = std::min(mi.m, mi.n);
+    mi.l = std::max(mi.m, mi.n);
+    mi.S = round_up(mi.s, kTile);
+    mi.L = round_up(mi.l, kTile);
+    mi.dtype = mats[i].param_dtype;
+    const int64_t pad_r = mi.tall ? mi.L : mi.S, pad_c = mi.tall ? mi.S : mi.L;
+    mi.tiles_pad_r = static_cast<int>(pad_r / kEwTile);
+    mi.tiles_pad_c = static_cast<int>(pad_c / kEwTile);
+    mi.tiles_upd_r = static_cast<int>((mi.m + kEwTile - 1) / kEwTile);
+    mi.tiles_upd_c = static_cast<int>((mi.n + kEwTile - 1) / kEwTile);
+    auto key = std::make_pair(mi.s, mi.l);
+    auto it = group_of.find(key);
+    if (it == group_of.end()) {
+      it = group_of.emplace(key, static_cast<int>(p->groups.size())).first;
+      GroupInfo g{};
+      g.s = mi.s;
+      g.l = mi.l;
+      g.S = mi.S;
+      g.L = mi.L;
+      p->groups.push_back(g);
+    }
+    mi.group = it->second;
+    mi.gidx = static_cast<int>(p->groups[mi.group].mats.size());
+    p->groups[mi.group].mats.push_back(i);
+  }
+  // Workspace layout: per-matrix scalars, then each group's NS buffers, then
+  // per-matrix partials and vectors.  Every region starts 256-byte aligned.
+  size_t off = 0;
+  p->off_scal = off;
+  off = align_up(off + sizeof(MatScalars) * static_cast<size_t>(count), kAlign);
+  for (GroupInfo& g : p->groups) {
+    const size_t c = g.mats.size();
+    g.stride_x = g.S * g.L;
+    g.stride_a = g.S * g.S;
+    g.stride_rpart = (g.L / kTile) * g.S;
+    g.stride_cpart = (g.S / kTile) * g.L;
+    g.off_fold = off;
+    off = align_up(off + 8 * c, kAlign);
+    g.off_xa = off;
+    off = align_up(off + 2 * c * g.stride_x, kAlign);
+    g.off_xb = off;
+    off = align_up(off + 2 * c * g.stride_x, kAlign);
+    g.off_a = off;
+    off = align_up(off + 2 * c * g.stride_a, kAlign);
+    g.off_p = off;
+    off = align_up(off + 2 * c * g.stride_a, kAlign);
+    g.off_rpart = off;
+    off = align_up(off + 4 * c * g.stride_rpart, kAlign);
+    g.off_cpart = off;
+    off = align_up(off + 4 * c * g.stride_cpart, kAlign);
+  }
+  for (MatInfo& mi : p->mats) {
+    mi.off_part = off;
+    off = align_up(off + 4 * static_cast<size_t>(mi.tiles_pad_r) * mi.tiles_pad_c, kAlign);
+    mi.off_rrms = off;
+    off = align_up(off + 8 * static_cast<size_t>(mi.m), kAlign);
+    mi.off_crms = off;
+    off = align_up(off + 8 * static_cast<size_t>(mi.n), kAlign);
+    mi.off_scale = off;
+    off = align_up(off + 4 * static_cast<size_t>(std::max(mi.m, mi.n)), kAlign);
+  }
+  p->ws_bytes = off;
+  *out = p;
+  return MEQ_OK;
+}
+
+MEQ_EXPORT size_t meq_workspace_bytes(const meq_plan* plan) { return plan ? plan->ws_bytes : 0; }
+
+MEQ_EXPORT int32_t meq_plan_num_groups(const meq_plan* plan) {
+  return plan ? static_cast<int32_t>(plan->groups.size()) : 0;
+}
+
+MEQ_EXPORT meq_status meq_plan_group(const meq_plan* plan, int32_t g, int64_t* s, int64_t* l, int32_t* count) {
+  if (!plan || g < 0 || g >= static_cast<int32_t>(plan->groups.size())) return MEQ_ERR_INVALID_ARG;
+  const GroupInfo& gi = plan->groups[g];
+  if (s) *s = gi.s;
+  if (l) *l = gi.l;
+  if (count) *count = static_cast<int32_t>(gi.mats.size());
+  return MEQ_OK;
+}
+
+MEQ_EXPORT meq_status meq_debug_region(const meq_plan* plan, int32_t matrix, int32_t kind, size_t* offset,
+                                       int64_t* rows, int64_t* cols, int64_t* ld) {
+  if (!plan || matrix < 0 || matrix >= static_cast<int32_t>(plan->mats.size())) return MEQ_ERR_INVALID_ARG;
+  const MatInfo& mi = plan->mats[matrix];
+  const GroupInfo& g = plan->groups[mi.group];
+  size_t o = 0;
+  int64_t r = 1, c = 1, d = 1;
+  switch (kind) {
+    case MEQ_BUF_X0:
+    case MEQ_BUF_U: {
+      // X_0 sits in buffer a; iteration k writes buffer b when k is even, so the
+      // output of K steps is in b for odd K and in a for even K.
+      const bool in_b = kind == MEQ_BUF_U && (plan->hp.ns_steps % 2 == 1);
+      o = (in_b ? g.off_xb : g.off_xa) + 2 * static_cast<size_t>(mi.gidx) * g.stride_x;
+      r = mi.s;
+      c = mi.l;
+      d = g.L;
+      break;
+    }
+    case MEQ_BUF_NORMSQ:
+      o = plan->off_scal + sizeof(MatScalars) * matrix + offsetof(MatScalars, normsq);
+      break;
+    case MEQ_BUF_ROW_RMS:
+      o = mi.off_rrms;
+      c = mi.m;
+      d = mi.m;
+      break;
+    case MEQ_BUF_COL_RMS:
+      o = mi.off_crms;
+      c = mi.n;
+      d = mi.n;
+      break;
+    case MEQ_BUF_SCALE:
+      o = mi.off_scale;
+      c = std::max(mi.m, mi.n);
+      d = c;
+      break;
+    default:
+      return MEQ_ERR_INVALID_ARG;
+  }
+  if (offset) *offset = o;
+  if (rows) *rows = r;
+  if (cols) *cols = c;
+  if (ld) *ld = d;
+  return MEQ_OK;
+}
+
+MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* const* grads, float* const* momenta,
+                               float lr, void* workspace, size_t workspace_bytes, hipStream_t st) {
+  if (!p) return MEQ_ERR_INVALID_ARG;
+  const int count = static_cast<int>(p->mats.size());
+  if (!std::isfinite(lr) || lr < 0.f) return MEQ_ERR_INVALID_ARG;
+  if (count == 0) return MEQ_OK;
+  if (!params || !grads || !momenta) return MEQ_ERR_INVALID_ARG;
+  for (int i = 0; i < count; ++i)
+    if (!params[i] || !grads[i] || !momenta[i]) return MEQ_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < p->ws_bytes || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return MEQ_ERR_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
+  const meq_hparams& hp = p->hp;
+
+  // Element-wise kernels run over chunks of matrices sharing a dtype.
+  std::vector<std::vector<int>> chunks;
+  for (int dt = 0; dt < 2; ++dt) {
+    std::vector<int> cur;
+    for (int i = 0; i < count; ++i) {
+      if (p->mats[i].dtype != dt) continue;
+      cur.push_back(i);
+      if (static_cast<int>(cur.size()) == kMaxChunk) {
+        chunks.push_back(cur);
+        cur.clear();
+      }
+    }
+    if (!cur.empty()) chunks.push_back(cur);
+  }
+
+  // 1. momentum + bf16 V (wide, zero-padded) + per-tile ||V||^2 partials
+  for (const auto& ch : chunks) {
+    MomentumArgs a{};
+    a.count = static_cast<int>(ch.size());
+    a.nesterov = hp.nesterov;
+    a.mu = hp.mu;
+    int tiles = 0;
+    for (int k = 0; k < a.count; ++k) {
+      const MatInfo& mi = p->mats[ch[k]];
+      const GroupInfo& g = p->groups[mi.group];
+      a.tile_start[k] = tiles;
+      tiles += mi.tiles_pad_r * mi.tiles_pad_c;
+      a.m[k] = static_cast<int>(mi.m);
+      a.n[k] = static_cast<int>(mi.n);
+      a.tiles_c[k] = mi.tiles_pad_c;
+      a.tall[k] = mi.tall;
+      a.ldx[k] = g.L;
+      a.g[k] = grads[ch[k]];
+      a.b[k] = momenta[ch[k]];
+      a.x[k] = reinterpret_cast<uint16_t*>(ws + g.off_xa) + mi.gidx * g.stride_x;
+      a.part[k] = reinterpret_cast<float*>(ws + mi.off_part);
+    }
+    a.tile_start[a.count] = tiles;
+    const int gbf = p->mats[ch[0]].dtype == MEQ_BF16;
+    MEQ_TRY(timed_launch(p, MEQ_K_MOMENTUM, st, [&] { return launch_momentum(a, gbf, tiles, st); }));
+  }
+  // 2. ||V||_F^2 and its reciprocals
+  for (int c0 = 0; c0 < count; c0 += kMaxChunk) {
+    NormArgs a{};
+    a.count = std::min(kMaxChunk, count - c0);
+    for (int k = 0; k < a.count; ++k) {
+      const MatInfo& mi = p->mats[c0 + k];
+      a.nparts[k] = mi.tiles_pad_r * mi.tiles_pad_c;
+      a.part[k] = reinterpret_cast<const float*>(ws + mi.off_part);
+      a.scal[k] = scal + c0 + k;
+      a.fold[k] = reinterpret_cast<float*>(ws + p->groups[mi.group].off_fold) + 2 * mi.gidx;
+    }
+    MEQ_TRY(timed_launch(p, MEQ_K_NORM, st, [&] { return launch_norm(a, st); }));
+  }
+  // 3. Newton-Schulz, batched per shape group (ping-pong between buffers a and b).
+  for (size_t gi = 0; gi < p->groups.size(); ++gi) {
+    const GroupInfo& g = p->groups[gi];
+    const int batch = static_cast<int>(g.mats.size());
+    const int tm = static_cast<int>(g.S / kTile), tn = static_cast<int>(g.L / kTile);
+    uint16_t* xa = reinterpret_cast<uint16_t*>(ws + g.off_xa);
+    uint16_t* xb = reinterpret_cast<uint16_t*>(ws + g.off_xb);
+    uint16_t* am = reinterpret_cast<uint16_t*>(ws + g.off_a);
+    uint16_t* pm = reinterpret_cast<uint16_t*>(ws + g.off_p);
+    const float* fold = reinterpret_cast<const float*>(ws + g.off_fold);
+    uint16_t* cur = xa;
+    uint16_t* nxt = xb;
+    for (int k = 0; k < hp.ns_steps; ++k) {
+      GemmArgs ga{};
+      ga.a = cur; ga.lda = g.L; ga.stride_a = g.stride_x;
+      ga.b = cur; ga.ldb = g.L; ga.stride_b = g.stride_x;
+      ga.c = am; ga.ldc = g.S; ga.stride_c = g.stride_a;
+      ga.e = nullptr;
+      ga.fold = fold; ga.scale_kind = k == 0 ? 2 : 0;
+      ga.alpha_e = 0.f; ga.alpha_acc = 1.f;
+      ga.M = static_cast<int>(g.S); ga.N = static_cast<int>(g.S); ga.K = static_cast<int>(g.L);
+      ga.tiles_m = tm; ga.tiles_n = tm; ga.tiles_per_mat = tm * (tm + 1) / 2; ga.batch = batch;
+      MEQ_TRY(timed_launch(p, MEQ_K_GRAM, st, [&] { return launch_gemm(ga, 0, st); }));
+
+      GemmArgs gp{};
+      gp.a = am; gp.lda = g.S; gp.stride_a = g.stride_a;
+      gp.b = am; gp.ldb = g.S; gp.stride_b = g.stride_a;
+      gp.c = pm; gp.ldc = g.S; gp.stride_c = g.stride_a;
+      gp.e = am; gp.lde = g.S; gp.stride_e = g.stride_a;
+      gp.fold = fold; gp.scale_kind = 0;
+      gp.alpha_e = hp.ns_b; gp.alpha_acc = hp.ns_c;
+      gp.M = static_cast<int>(g.S); gp.N = static_cast<int>(g.S); gp.K = static_cast<int>(g.S);
+      gp.tiles_m = tm; gp.tiles_n = tm; gp.tiles_per_mat = tm * (tm + 1) / 2; gp.batch = batch;
+      MEQ_TRY(timed_launch(p, MEQ_K_POLY, st, [&] { return launch_gemm(gp, 1, st); }));
+
+      GemmArgs gx{};
+      gx.a = pm; gx.lda = g.S; gx.stride_a = g.stride_a;
+      gx.b = cur; gx.ldb = g.L; gx.stride_b = g.stride_x;
+      gx.c = nxt; gx.ldc = g.L; gx.stride_c = g.stride_x;
+      gx.e = cur; gx.lde = g.L; gx.stride_e = g.stride_x;
+      gx.fold = fold; gx.scale_kind = k == 0 ? 1 : 0;
+      gx.alpha_e = hp.ns_a; gx.alpha_acc = 1.f;
+      gx.M = static_cast<int>(g.S); gx.N = static_cast<int>(g.L); gx.K = static_cast<int>(g.S);
+      gx.tiles_m = tm; gx.tiles_n = tn; gx.tiles_per_mat = tm * tn; gx.batch = batch;
+      MEQ_TRY(timed_launch(p, MEQ_K_APPLY, st, [&] { return launch_gemm(gx, 2, st); }));
+      std::swap(cur, nxt);
+    }
+    // 4. row / column sums of squares of U
+    RowColArgs rc{};
+    rc.u = (hp.ns_steps % 2 == 1) ? xb : xa;
+    rc.stride_u = g.stride_x;
+    rc.S = static_cast<int>(g.S);
+    rc.L = static_cast<int>(g.L);
+    rc.rpart = reinterpret_cast<float*>(ws + g.off_rpart);
+    rc.stride_rpart = g.stride_rpart;
+    rc.cpart = reinterpret_cast<float*>(ws + g.off_cpart);
+    rc.stride_cpart = g.stride_cpart;
+    rc.tiles_r = tm;
+    rc.tiles_c = tn;
+    MEQ_TRY(timed_launch(p, MEQ_K_ROWCOL, st, [&] { return launch_rowcol(rc, batch, st); }));
+  }
+  // 5. CVs, direction, scale vectors
+  for (int c0 = 0; c0 < count; c0 += kMaxChunk) {
+    SelectArgs a{};
+    a.count = std::min(kMaxChunk, count - c0);
+    a.delta = static_cast<double>(hp.zero_rms_delta);
+    for (int k = 0; k < a.count; ++k) {
+      const MatInfo& mi = p->mats[c0 + k];
+      const GroupInfo& g = p->groups[mi.group];
+      a.m[k] = static_cast<int>(mi.m);
+      a.n[k] = static_cast<int>(mi.n);
+      a.tall[k] = mi.tall;
+      a.S[k] = static_cast<int>(g.S);
+      a.L[k] = static_cast<int>(g.L);
+      a.rpart[k] = reinterpret_cast<const float*>(ws + g.off_rpart) + mi.gidx * g.stride_rpart;
+      a.cpart[k] = reinterpret_cast<const float*>(ws + g.off_cpart) + mi.gidx * g.stride_cpart;
+      a.rrms[k] = reinterpret_cast<double*>(ws + mi.off_rrms);
+      a.crms[k] = reinterpret_cast<double*>(ws + mi.off_crms);
+      a.scale[k] = reinterpret_cast<float*>(ws + mi.off_scale);
+      a.scal[k] = scal + c0 + k;
+    }
+    MEQ_TRY(timed_launch(p, MEQ_K_SELECT, st, [&] { return launch_select(a, st); }));
+  }
+  // 6. write-back
+  const float decay = static_cast<float>(1.0 - static_cast<double>(lr) * hp.weight_decay);
+  const float stepc = static_cast<float>(static_cast<double>(hp.rho) * lr);
+  for (const auto& ch : chunks) {
+    UpdateArgs a{};
+    a.count = static_cast<int>(ch.size());
+    a.decay = decay;
+    a.step = stepc;
+    int tiles = 0;
+    for (int k = 0; k < a.count; ++k) {
+      const MatInfo& mi = p->mats[ch[k]];
+      const GroupInfo& g = p->groups[mi.group];
+      a.tile_start[k] = tiles;
+      tiles += mi.tiles_upd_r * mi.tiles_upd_c;
+      a.m[k] = static_cast<int>(mi.m);
+      a.n[k] = static_cast<int>(mi.n);
+      a.tiles_c[k] = mi.tiles_upd_c;
+      a.tall[k] = mi.tall;
+      a.ldu[k] = g.L;
+      a.w[k] = params[ch[k]];
+      const size_t uoff = (hp.ns_steps % 2 == 1) ? g.off_xb : g.off_xa;
+      a.u[k] = reinterpret_cast<const uint16_t*>(ws + uoff) + mi.gidx * g.stride_x;
+      a.scale[k] = reinterpret_cast<const float*>(ws + mi.off_scale);
+      a.scal[k] = scal + ch[k];
+    }
+    a.tile_start[a.count] = tiles;
+    const int pbf = p->mats[ch[0]].dtype == MEQ_BF16;
+    MEQ_TRY(timed_launch(p, MEQ_K_UPDATE, st, [&] { return launch_update(a, pbf, tiles, st); }));
+  }
+  return MEQ_OK;
+}
+
+MEQ_EXPORT meq_status meq_get_stats(const meq_plan* plan, const void* workspace, double* gamma_r, double* gamma_c,
+                                    int32_t* dir, hipStream_t st) {
+  if (!plan) return MEQ_ERR_INVALID_ARG;
+  const size_t count = plan->mats.size();
+  if (count == 0) return MEQ_OK;
+  if (!workspace) return MEQ_ERR_WORKSPACE;
+  std::vector<MatScalars> host(count);
+  const char* src = static_cast<const char*>(workspace) + plan->off_scal;
+  if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
+    return MEQ_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;
+  for (size_t i = 0; i < count; ++i) {
+    if (gamma_r) gamma_r[i] = host[i].gamma_r;
+    if (gamma_c) gamma_c[i] = host[i].gamma_c;
+    if (dir) dir[i] = host[i].dir;
+  }
+  return MEQ_OK;
+}
+
+MEQ_EXPORT meq_status meq_set_timing(meq_plan* plan, uint32_t kind_mask) {
+  if (!plan) return MEQ_ERR_INVALID_ARG;
+  plan->timing_mask = kind_mask & ((1u << MEQ_K_COUNT) - 1);
+  return MEQ_OK;
+}
+
+MEQ_EXPORT meq_status meq_get_timing(meq_plan* plan, int32_t kind, double* total_ms, int64_t* launches,
+                                     int32_t reset) {
+  if (!plan || kind < 0 || kind >= MEQ_K_COUNT) return MEQ_ERR_INVALID_ARG;
+  for (const TimedLaunch& tl : plan->pending) {
+    if (hipEventSynchronize(tl.stop) != hipSuccess) return MEQ_ERR_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, tl.start, tl.stop) != hipSuccess) return MEQ_ERR_HIP;
+    plan->total_ms[tl.kind] += ms;
+    plan->launches[tl.kind] += 1;
+    plan->event_pool.push_back(tl.start);
+    plan->event_pool.push_back(tl.stop);
+  }
+  plan->pending.clear();
+  if (total_ms) *total_ms = plan->total_ms[kind];
+  if (launches) *launches = plan->launches[kind];
+  if (reset) {
+    for (int k = 0; k < MEQ_K_COUNT; ++k) {
+      plan->total_ms[k] = 0.0;
+      plan->launches[k] = 0;
+    }
+  }
+  return MEQ_OK;
+}
+
+MEQ_EXPORT void meq_destroy(meq_plan* plan) {
+  if (!plan) return;
+  for (const TimedLaunch& tl : plan->pending) {
+    hipEventDestroy(tl.start);
+    hipEventDestroy(tl.stop);
+  }
+  for (hipEvent_t e : plan->event_pool) hipEventDestroy(e);
+  delete plan;
+}

@@ -1,0 +1,124 @@
+// Internal definitions shared by the host planner and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace meq {
+
+// Every Newton-Schulz buffer is padded to multiples of this tile on both sides,
+// so the GEMM kernels never need bounds checks.  Zero padding is exact for the
+// iteration: zero rows/columns of X stay zero through X X^T, A A and P X.
+constexpr int kTile = 256;
+// Element-wise kernels work on 64 x 64 tiles of the matrix's own orientation.
+constexpr int kEwTile = 64;
+// Matrices per launch of the multi-matrix element-wise kernels (pointers travel as kernel arguments).
+constexpr int kMaxChunk = 32;
+
+// Per-matrix scalars kept at the start of the workspace.
+struct MatScalars {
+  double normsq;   // ||V||_F^2
+  double gamma_r;  // CV of row RMS of U
+  double gamma_c;  // CV of column RMS of U
+  float inv_norm;  // 1 / ||V||_F  (0 for a zero matrix)
+  float inv_normsq;
+  int32_t dir;     // 0 row, 1 column
+  int32_t pad;
+};
+static_assert(sizeof(MatScalars) == 40, "layout");
+
+// ----------------------------------------------------------------- momentum + bf16 V
+struct MomentumArgs {
+  int count;
+  int nesterov;
+  float mu;
+  int tile_start[kMaxChunk + 1];  // prefix sum of 64x64 tiles over the padded matrix
+  int m[kMaxChunk], n[kMaxChunk];
+  int tiles_c[kMaxChunk];         // 64-wide tile columns of the padded matrix (own orientation)
+  int tall[kMaxChunk];
+  int64_t ldx[kMaxChunk];         // leading dimension of the wide bf16 buffer (padded long side)
+  const void* g[kMaxChunk];
+  float* b[kMaxChunk];
+  uint16_t* x[kMaxChunk];         // wide bf16 V, padded
+  float* part[kMaxChunk];         // one sum of squares per tile
+};
+
+// --------------------------------------------------------------------- norm finalize
+struct NormArgs {
+  int count;
+  int nparts[kMaxChunk];
+  const float* part[kMaxChunk];
+  MatScalars* scal[kMaxChunk];
+  float* fold[kMaxChunk];  // (1/||V||, 1/||V||^2) at the matrix's slot of its shape group
+};
+
+// ------------------------------------------------------------------------ NS GEMMs
+// C = s * (alpha_e * E + alpha_acc * (Aop . Bop)) stored as bf16, batched over
+// the matrices of one shape group.  Aop is M x K row-major.  Bop is N x K
+// row-major (NT) or K x N row-major (NN).  For the symmetric products only tiles
+// on or above the diagonal are computed and each off-diagonal tile is also
+// stored mirrored.
+struct GemmArgs {
+  const uint16_t* a;
+  int64_t lda, stride_a;
+  const uint16_t* b;
+  int64_t ldb, stride_b;
+  uint16_t* c;
+  int64_t ldc, stride_c;
+  const uint16_t* e;  // may be null when alpha_e == 0
+  int64_t lde, stride_e;
+  const float* fold;  // per batch member: (1/||V||, 1/||V||^2)
+  int scale_kind;     // 0 none, 1 scale by 1/||V||, 2 scale by 1/||V||^2
+  float alpha_e, alpha_acc;
+  int M, N, K;
+  int tiles_m, tiles_n, tiles_per_mat, batch;
+};
+
+// ----------------------------------------------------------------- row/col sums of U
+struct RowColArgs {
+  const uint16_t* u;  // group base, wide, S x L per matrix
+  int64_t stride_u;
+  int S, L;
+  float* rpart;  // per matrix: (L/256) x S
+  int64_t stride_rpart;
+  float* cpart;  // per matrix: (S/256) x L
+  int64_t stride_cpart;
+  int tiles_r, tiles_c;
+};
+
+// ------------------------------------------------------------------ CV + direction
+struct SelectArgs {
+  int count;
+  double delta;
+  int m[kMaxChunk], n[kMaxChunk], tall[kMaxChunk], S[kMaxChunk], L[kMaxChunk];
+  const float* rpart[kMaxChunk];
+  const float* cpart[kMaxChunk];
+  double* rrms[kMaxChunk];
+  double* crms[kMaxChunk];
+  float* scale[kMaxChunk];
+  MatScalars* scal[kMaxChunk];
+};
+
+// ------------------------------------------------------------------------ write-back
+struct UpdateArgs {
+  int count;
+  float decay;  // 1 - lr * lambda
+  float step;   // rho * lr
+  int tile_start[kMaxChunk + 1];
+  int m[kMaxChunk], n[kMaxChunk], tiles_c[kMaxChunk], tall[kMaxChunk];
+  int64_t ldu[kMaxChunk];
+  void* w[kMaxChunk];
+  const uint16_t* u[kMaxChunk];
+  const float* scale[kMaxChunk];
+  const MatScalars* scal[kMaxChunk];
+};
+
+// Launchers (defined in the .hip files).  Each returns the hipError_t of the launch.
+hipError_t launch_momentum(const MomentumArgs& a, int grad_bf16, int total_tiles, hipStream_t st);
+hipError_t launch_norm(const NormArgs& a, hipStream_t st);
+hipError_t launch_gemm(const GemmArgs& a, int mode, hipStream_t st);  // 0 Gram, 1 poly, 2 apply
+hipError_t launch_rowcol(const RowColArgs& a, int batch, hipStream_t st);
+hipError_t launch_select(const SelectArgs& a, hipStream_t st);
+hipError_t launch_update(const UpdateArgs& a, int param_bf16, int total_tiles, hipStream_t st);
+
+}  // namespace meq

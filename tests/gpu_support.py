@@ -1,0 +1,156 @@
+"""Shared helpers of the GPU parity tests (not a test module)."""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+import workloads
+from paper_2609_35701_amd import meq
+
+# Stated tolerances (relative Frobenius errors):
+TOL_FP32 = 1e-5     # fp32 element-wise and reduction stages
+TOL_NS = 3e-2       # bf16 Newton-Schulz output
+TOL_DELTA = 3e-2    # final parameter delta
+TIE_TAU = 0.05      # |gamma_r - gamma_c| <= tau * max(...) on the oracle's own U: either direction is correct
+TIE_TAU_STAGE = 1e-5  # same rule when the oracle is fed the GPU's own U
+
+DEV = "cuda:0"
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def relerr(a, b) -> float:
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    nb = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (nb if nb > 0 else 1.0))
+
+
+def oracle_hp(hp: meq.HParams) -> oracle.HParams:
+    """The oracle's hyperparameters: the float32 values the C boundary holds, in float64."""
+    return oracle.HParams(float(np.float32(hp.mu)), float(np.float32(hp.rho)), float(np.float32(hp.weight_decay)),
+                          int(hp.ns_steps), float(np.float32(hp.ns_a)), float(np.float32(hp.ns_b)),
+                          float(np.float32(hp.ns_c)), float(np.float32(hp.zero_rms_delta)), bool(hp.nesterov))
+
+
+def to_dev(x: np.ndarray, dtype: str) -> torch.Tensor:
+    t = torch.from_numpy(np.ascontiguousarray(x, np.float32))
+    t = t.to(torch.bfloat16) if dtype == "bf16" else t
+    return t.to(DEV).contiguous()
+
+
+def to_np(t: torch.Tensor) -> np.ndarray:
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def wide(x: np.ndarray) -> np.ndarray:
+    return x.T if x.shape[0] > x.shape[1] else x
+
+
+def ulp_bf16(x: np.ndarray) -> np.ndarray:
+    """Spacing of bfloat16 numbers at |x| (8 significant bits)."""
+    x = np.abs(np.asarray(x, np.float64))
+    _, e = np.frexp(np.where(x > 0, x, 1.0))
+    return np.ldexp(1.0, np.maximum(e, -125) - 8)
+
+
+class Run:
+    """Matrices of a workload on the GPU, stepped through the HIP path."""
+
+    def __init__(self, wl: workloads.Workload, idxs, hp: meq.HParams | None = None):
+        self.wl = wl
+        self.idxs = list(idxs)
+        self.hp = hp if hp is not None else meq.default_hparams()
+        self.w0 = [workloads.weight_init(wl, i) for i in self.idxs]
+        self.params = [to_dev(w, wl.param_dtype) for w in self.w0]
+        self.upd = meq.HiddenWeightUpdate(self.params, self.hp)
+        self.step_no = 0
+
+    def grads(self, step: int):
+        return [workloads.grad_at_step(self.wl, i, step) for i in self.idxs]
+
+    def step(self, lr: float, grads_np=None):
+        grads_np = self.grads(self.step_no) if grads_np is None else grads_np
+        g_dev = [to_dev(g, self.wl.param_dtype) for g in grads_np]
+        self.upd.step(g_dev, lr)
+        torch.cuda.synchronize()
+        self.step_no += 1
+        return grads_np
+
+
+def check_direction(gpu_dir: int, gr: float, gc: float, tau: float) -> bool:
+    """True when the GPU's direction is acceptable for the oracle's CVs (ties within tau accept both)."""
+    want = oracle.ROW if gr >= gc else oracle.COL
+    if gpu_dir == want:
+        return True
+    return abs(gr - gc) <= tau * max(gr, gc)
+
+
+def check_matrix_step(run: Run, k: int, w_before: np.ndarray, b_before: np.ndarray, g: np.ndarray, lr: float,
+                      gpu_stats, label: str):
+    """Stage-by-stage and end-to-end parity of one matrix after one GPU step."""
+    hp = oracle_hp(run.hp)
+    upd = run.upd
+    gr_gpu, gc_gpu, dir_gpu = gpu_stats[0][k], gpu_stats[1][k], gpu_stats[2][k]
+    # a1: momentum (fp32)
+    b_gpu = to_np(upd.momenta[k])
+    b_or = oracle.momentum(b_before, g, hp.mu)
+    assert relerr(b_gpu, b_or) <= TOL_FP32, f"{label}: momentum {relerr(b_gpu, b_or)}"
+    # a2: ||V||^2 and bf16 V (wide)
+    v_or = oracle.ns_input(b_or, g, hp.mu, hp.nesterov)
+    nsq_gpu = float(upd.view(k, meq.BUF_NORMSQ).cpu()[0])
+    nsq_or = float(np.sum(v_or * v_or))
+    assert abs(nsq_gpu - nsq_or) <= TOL_FP32 * max(nsq_or, 1e-300), f"{label}: normsq {nsq_gpu} vs {nsq_or}"
+    x0_gpu = to_np(upd.view(k, meq.BUF_X0))
+    x0_or = oracle.round_bf16(wide(v_or))
+    diff = np.abs(x0_gpu - x0_or)
+    assert np.all(diff <= ulp_bf16(x0_or) + 1e-300), f"{label}: bf16 V off by more than one ulp"
+    # a3: Newton-Schulz on the GPU's own X0 (and on the oracle's V)
+    u_gpu_w = to_np(upd.view(k, meq.BUF_U))
+    u_gpu = u_gpu_w.T if w_before.shape[0] > w_before.shape[1] else u_gpu_w
+    u_or_same = oracle.newton_schulz(x0_gpu, hp.ns_a, hp.ns_b, hp.ns_c, hp.ns_steps)
+    e_ns = relerr(u_gpu_w, u_or_same)
+    assert e_ns <= TOL_NS, f"{label}: NS error {e_ns}"
+    # a4/a5 on the GPU's U: r, c, CVs, direction, scale
+    r_or, c_or = oracle.row_col_rms(u_gpu)
+    r_gpu = to_np(upd.view(k, meq.BUF_ROW_RMS))
+    c_gpu = to_np(upd.view(k, meq.BUF_COL_RMS))
+    assert relerr(r_gpu, r_or) <= TOL_FP32 and relerr(c_gpu, c_or) <= TOL_FP32, f"{label}: row/col RMS"
+    _, gr_s, gc_s, d_s = oracle.equilibrate(u_gpu, hp.delta)
+    assert abs(gr_gpu - gr_s) <= TOL_FP32 * max(gr_s, 1e-3) and abs(gc_gpu - gc_s) <= TOL_FP32 * max(gc_s, 1e-3), \
+        f"{label}: CVs {gr_gpu, gc_gpu} vs {gr_s, gc_s}"
+    assert check_direction(dir_gpu, gr_s, gc_s, TIE_TAU_STAGE), f"{label}: direction {dir_gpu} vs {d_s}"
+    ut_stage, _, _, _ = oracle.equilibrate(u_gpu, hp.delta, force_dir=dir_gpu)
+    sc_gpu = to_np(upd.view(k, meq.BUF_SCALE))
+    ref = r_or if dir_gpu == oracle.ROW else c_or
+    want_sc = np.where(ref > hp.delta, 1.0 / np.where(ref > hp.delta, ref, 1.0), 0.0)
+    assert relerr(sc_gpu[:ref.size], want_sc) <= TOL_FP32, f"{label}: scale vector"
+    # a6: write-back given the GPU's U
+    w_gpu = to_np(run.params[k])
+    w_stage = oracle.write_back(w_before, ut_stage, lr, hp.rho, hp.weight_decay)
+    if run.wl.param_dtype == "bf16":
+        w_rne = oracle.round_bf16(w_stage)
+        off = np.abs(w_gpu - w_rne)
+        assert np.all(off <= ulp_bf16(w_rne) + 1e-300), f"{label}: bf16 W more than 1 ulp off"
+        exact = float(np.mean(off == 0))
+        assert exact >= 0.999, f"{label}: only {exact:.5f} of bf16 W exact"
+    else:
+        assert relerr(w_gpu - w_before, w_stage - w_before) <= TOL_FP32, f"{label}: fp32 write-back"
+    # end to end against the oracle's own fp64 step (R8 rule for near ties)
+    full = oracle.meq_step(w_before, g, b_before, hp, lr, wide=True)
+    e_u = relerr(u_gpu, full["U"])
+    assert e_u <= TOL_NS, f"{label}: NS end-to-end {e_u}"
+    assert check_direction(dir_gpu, full["gamma_r"], full["gamma_c"], TIE_TAU), \
+        f"{label}: direction {dir_gpu} vs oracle CVs {full['gamma_r'], full['gamma_c']}"
+    if dir_gpu != full["dir"]:
+        full = oracle.meq_step(w_before, g, b_before, hp, lr, force_dir=dir_gpu, wide=True)
+    e_d = relerr(w_gpu - w_before, full["W"] - w_before)
+    assert e_d <= TOL_DELTA, f"{label}: parameter delta {e_d}"
+    return {"ns": e_ns, "ns_e2e": e_u, "delta": e_d, "dir": dir_gpu, "tie": dir_gpu != d_s}
