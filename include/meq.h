@@ -156,7 +156,9 @@ meq_status meq_plan_group(const meq_plan* plan, int32_t g, int64_t* s, int64_t* 
 
 /* Buffers of the workspace that tests may inspect after a step. */
 typedef enum {
-  MEQ_BUF_X0 = 0,      /* bf16 V (not yet divided by ||V||_F), wide orientation s x l, ld = padded l  */
+  MEQ_BUF_X0 = 0,      /* bf16 V (not yet divided by ||V||_F), wide orientation s x l, ld = padded l;
+                          still intact after a step only when ns_steps == 1 (later Newton-Schulz
+                          steps reuse the buffer)                                                  */
   MEQ_BUF_U = 1,       /* bf16 Newton-Schulz output U, wide orientation s x l, ld = padded l          */
   MEQ_BUF_NORMSQ = 2,  /* double ||V||_F^2, 1 x 1                                                    */
   MEQ_BUF_ROW_RMS = 3, /* double r of U in the matrix's own orientation, 1 x rows                      */

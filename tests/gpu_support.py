@@ -108,10 +108,16 @@ def check_matrix_step(run: Run, k: int, w_before: np.ndarray, b_before: np.ndarr
     nsq_gpu = float(upd.view(k, meq.BUF_NORMSQ).cpu()[0])
     nsq_or = float(np.sum(v_or * v_or))
     assert abs(nsq_gpu - nsq_or) <= TOL_FP32 * max(nsq_or, 1e-300), f"{label}: normsq {nsq_gpu} vs {nsq_or}"
-    x0_gpu = to_np(upd.view(k, meq.BUF_X0))
     x0_or = oracle.round_bf16(wide(v_or))
-    diff = np.abs(x0_gpu - x0_or)
-    assert np.all(diff <= ulp_bf16(x0_or) + 1e-300), f"{label}: bf16 V off by more than one ulp"
+    if run.hp.ns_steps == 1:
+        # the X_0 buffer survives the step only with one Newton-Schulz step
+        x0_gpu = to_np(upd.view(k, meq.BUF_X0))
+        diff = np.abs(x0_gpu - x0_or)
+        assert np.all(diff <= ulp_bf16(x0_or) + 1e-300), f"{label}: bf16 V off by more than one ulp"
+    else:
+        # the GPU's X_0 is the round-to-nearest-even bf16 image of its fp32 V, which equals the
+        # rounded fp64 V except at rare rounding ties (checked bit for bit in the one-step test)
+        x0_gpu = x0_or
     # a3: Newton-Schulz on the GPU's own X0 (and on the oracle's V)
     u_gpu_w = to_np(upd.view(k, meq.BUF_U))
     u_gpu = u_gpu_w.T if w_before.shape[0] > w_before.shape[1] else u_gpu_w
@@ -136,9 +142,16 @@ def check_matrix_step(run: Run, k: int, w_before: np.ndarray, b_before: np.ndarr
     w_gpu = to_np(run.params[k])
     w_stage = oracle.write_back(w_before, ut_stage, lr, hp.rho, hp.weight_decay)
     if run.wl.param_dtype == "bf16":
+        # One bf16 ulp of the rounded value, plus the fp32 evaluation error of
+        # decay * W - rho * lr * u * s (a few fp32 ulps of its terms), which only
+        # matters where the two terms cancel to almost zero.
         w_rne = oracle.round_bf16(w_stage)
         off = np.abs(w_gpu - w_rne)
-        assert np.all(off <= ulp_bf16(w_rne) + 1e-300), f"{label}: bf16 W more than 1 ulp off"
+        fp32_err = 2.0 ** -21 * (np.abs(w_before) + hp.rho * lr * np.abs(ut_stage))
+        bound = ulp_bf16(w_rne) + fp32_err
+        bad = off > bound
+        assert not np.any(bad), (f"{label}: {int(bad.sum())} bf16 W beyond 1 ulp + fp32 error, worst at "
+                                 f"|W'|={np.abs(w_rne[bad]).min():.3g}, off={off[bad].max():.3g}")
         exact = float(np.mean(off == 0))
         assert exact >= 0.999, f"{label}: only {exact:.5f} of bf16 W exact"
     else:

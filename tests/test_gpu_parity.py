@@ -42,6 +42,14 @@ def test_single_matrix_256x512_fp32():
     run_and_check(workloads.workload("single-256x512"), [0], label="single-256x512")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_one_ns_step_keeps_x0(dtype):
+    """With K = 1 the bf16 V buffer survives: V within one bf16 ulp of the rounded oracle V,
+    and one Newton-Schulz step on exactly that X_0 matches the oracle."""
+    wl = workloads.custom([(200, 72), (72, 200), (256, 512)], dtype, name=f"one-step-{dtype}")
+    run_and_check(wl, [0, 1, 2], steps=2, hp=meq.default_hparams(ns_steps=1), label=wl.name)
+
+
 def test_llama130m_subset_ten_steps():
     wl = workloads.workload("llama-130m")
     # q, k, v, o, gate, up, down of layer 0 and the down projection of the last layer
@@ -104,9 +112,12 @@ def test_signed_permutation_closed_form(shape):
     w0 = to_np(run.params[0])
     run.step(LR, [np.float32(0.25) * q])
     gr, gc, d = run.upd.stats()
-    assert gr == [0.0] and gc == [0.0] and d == [oracle.ROW]  # exact tie selects rows
+    # both CVs vanish (up to the rounding of a mean of equal values): a tie, where rows and
+    # columns are both correct choices; U~ = sqrt(n) Q for rows, sqrt(m) Q for columns
+    assert max(gr[0], gc[0]) < 1e-12
     hp = oracle_hp(run.hp)
-    want = oracle.write_back(w0, np.sqrt(n) * q.astype(np.float64), LR, hp.rho, hp.weight_decay)
+    scale = np.sqrt(n) if d[0] == oracle.ROW else np.sqrt(m)
+    want = oracle.write_back(w0, scale * q.astype(np.float64), LR, hp.rho, hp.weight_decay)
     assert relerr(to_np(run.params[0]) - w0, want - w0) <= 1e-5
 
 
@@ -121,9 +132,13 @@ def test_zero_rows_and_columns_stay_zero():
     run.step(LR, [g])
     u = to_np(run.upd.view(0, meq.BUF_U))
     assert not np.any(u[[3, 77]]) and not np.any(u[:, 100:130])
-    dw = to_np(run.params[0]) - w0 * np.float32(1 - np.float32(LR) * np.float32(0.1))
+    hp = oracle_hp(run.hp)
+    decay = np.float32(1.0 - np.float64(np.float32(LR)) * np.float64(hp.weight_decay))
+    decayed = (np.float32(w0) * decay).astype(np.float64)
+    w1 = to_np(run.params[0])
     # zero rows/columns of U are zero in either direction's U~, so only decay reaches them
-    assert np.abs(dw[[3, 77]]).max() < 1e-9 and np.abs(dw[:, 100:130]).max() < 1e-9
+    np.testing.assert_array_equal(w1[[3, 77]], decayed[[3, 77]])
+    np.testing.assert_array_equal(w1[:, 100:130], decayed[:, 100:130])
 
 
 def test_bitwise_determinism():
@@ -186,7 +201,7 @@ def test_full_1b_launch_sampled_parity():
         groups.setdefault((min(s), max(s)), []).append(i)
     sample = sorted({g[0] for g in groups.values()} | {g[-1] for g in groups.values()})
     log(f"[case] llama-1b full launch, sampled matrices {sample}")
-    params, grads, moms = workloads.device_inputs(wl, DEV)
+    params, grads, _ = workloads.device_inputs(wl, DEV)
     w_np, g_np = {}, {}
     for i in sample:
         w_np[i] = workloads.weight_init(wl, i)
@@ -214,4 +229,4 @@ def test_full_1b_launch_sampled_parity():
     for i in range(wl.count):
         assert torch.isfinite(params[i].float()).all()
         assert gr[i] >= 0 and gc[i] >= 0
-    assert torch.equal(moms[5], grads[5].float())
+    assert torch.equal(upd.momenta[5], grads[5].float())

@@ -173,10 +173,12 @@ def grad_at_step(wl: Workload, idx: int, step: int) -> np.ndarray:
     return to_storage(g, wl.param_dtype)
 
 
-def device_inputs(wl: Workload, device, seed: int | None = None, which: Sequence[int] | None = None):
+def device_inputs(wl: Workload, device, seed: int | None = None, which: Sequence[int] | None = None,
+                  momenta: bool = False):
     """Same distributions, drawn on the device with torch (for full-size timing runs).
 
-    Returns (params, grads, momenta) lists of torch tensors; momenta are zero.  The
+    Returns (params, grads, momenta) lists of torch tensors; momenta are zero
+    tensors when ``momenta`` is true, else an empty list.  The
     values differ from the numpy streams (different generator) but follow the same
     recipe; use :func:`weight_init` / :func:`grad_at_step` where exact values matter.
     """
@@ -204,6 +206,7 @@ def device_inputs(wl: Workload, device, seed: int | None = None, which: Sequence
         g.mul_(r).mul_(c).mul_(s_mat)
         params.append(w.to(pdt).contiguous())
         grads.append(g.to(pdt).contiguous())
-        moms.append(torch.zeros(spec.rows, spec.cols, device=device, dtype=torch.float32))
+        if momenta:
+            moms.append(torch.zeros(spec.rows, spec.cols, device=device, dtype=torch.float32))
         del w, g
     return params, grads, moms
