@@ -1,16 +1,18 @@
 // Newton-Schulz products on bf16 MFMA (gfx950), eq. "ns":
-//   A_k = X_k X_k^T                (NT, symmetric output: upper tiles + mirrored store)
+//   A_k = X_k X_k^T                (NT, symmetric: tiles on or above the diagonal + mirrored store)
 //   P_k = b A_k + c A_k A_k        (NT since A_k is symmetric; symmetric output)
-//   X_{k+1} = a X_k + P_k X_k      (NN: X_k is read K-major and transposed in registers)
+//   X_{k+1} = a X_k + P_k X_k      (NN: X_k is staged K-major and read with LDS transpose reads)
 // X_0 = V / ||V||_F is folded in: the bf16 buffer holds V, the k = 0 Gram epilogue
 // scales by 1/||V||^2 and the k = 0 apply epilogue by 1/||V||.
 //
 // One workgroup = 4 waves = one 256 x 256 output tile; each wave owns a 128 x 128
-// quadrant as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation).  K
-// advances in slabs of 64 through double-buffered LDS (one barrier per slab);
-// the next slab's global loads are in flight while the current slab's MFMAs run.
-// A batch of same-shape matrices is one launch; workgroup ids are remapped so
-// consecutive tiles of one matrix run on one XCD (shared L2).
+// quadrant as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation in AGPRs).
+// K advances in slabs of 64.  Global -> LDS traffic uses buffer loads that write
+// LDS directly (no registers, no LDS store instructions), double-buffered, with
+// 16-byte chunks XOR-swizzled so that fragment reads are bank-conflict free.
+// The epilogue stages the output tile (and the tile it adds, X or A) in LDS and
+// writes whole rows with 16-byte stores.  Same-shape matrices form one launch;
+// workgroup ids are remapped so each XCD receives a contiguous run of tiles.
 #include "meq_internal.h"
 
 namespace meq {
@@ -18,27 +20,32 @@ namespace meq {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
-constexpr int BM = kTile, BN = kTile, BK = 64;
-constexpr int PK = BK + 8;  // LDS row pitch (elements): 144 B rows keep 16-byte fragment reads conflict-free
-constexpr int kOperandElems = BM * PK;
+constexpr int BK = 64;
+constexpr int kBufBytes = 65536;  // one LDS buffer: operand A slab (32 KiB) + operand B slab (32 KiB)
 // Buffer resource word 3 for raw (untyped, 32-bit format) buffer access on gfx9.
 constexpr int kBufferFlags = 0x00020000;
 
-__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
 
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> packed bf16 pair (v_cvt_pk_bf16_f32: round to nearest even), lo first.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+  return __builtin_bit_cast(uint32_t, v);
 }
-
-// Component q (a compile-time constant after unrolling) of a 4-dword vector.
-__device__ __forceinline__ uint32_t dword(const u32x4& v, int q) { return v[q]; }
 
 // Map a launch-order workgroup id to a logical tile so that the workgroups one
 // XCD receives (ids x, x + 8, x + 16, ... are dispatched round-robin over the 8
@@ -49,18 +56,35 @@ __device__ __forceinline__ int xcd_remap(int w, int nblk) {
   return x * q + min(x, r) + pos;
 }
 
-// kMode: 0 Gram (NT, symmetric, no epilogue input), 1 polynomial (NT, symmetric,
-// epilogue reads A), 2 apply (NN, epilogue reads X).
+// 16 bytes per lane from a buffer straight into LDS at dst + 16 * lane.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, lds_u8* dst, int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)dst, 16, voff, soff, 0, 0);
+}
+
+// s_waitcnt vmcnt(0) (expcnt and lgkmcnt left at their maxima).
+__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
+// LDS layouts (bytes):
+//   NT slab (256 rows x 64 k):  row r at r * 128; 16-byte chunk c (k = 8c..8c+7) at slot c ^ (r & 7).
+//   NN slab (64 k x 256 n):     row k at k * 512; chunk c (n = 8c..8c+7) at slot c ^ (2 (k & 3)).
+//   staged output half (128 x 256): row r at r * 512; chunk c at slot c ^ (r & 31).
+__device__ __forceinline__ int stage_byte(int rr, int c) { return rr * 512 + 16 * ((c >> 3) ^ (rr & 31)) + 2 * (c & 7); }
+
 template <int kMode>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_ns_gemm(GemmArgs g) {
   constexpr bool kNN = kMode == 2;
   constexpr bool kSym = kMode != 2;
   constexpr bool kHasE = kMode != 0;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kOperandElems];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds0_[kBufBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds1_[kBufBytes];
+  lds_u8* const lds0 = (lds_u8*)lds0_;
+  lds_u8* const lds1 = (lds_u8*)lds1_;
 
   const int t = threadIdx.x;
-  const int lane = t & 63, wave = t >> 6;
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // wave-uniform: scalar offsets and LDS bases
   const int wm = wave >> 1, wn = wave & 1;
+  const int h = lane >> 5;
 
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int mat = logical / g.tiles_per_mat;
@@ -86,54 +110,60 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     tj = in / gm;
   }
 
-  // Operands are read with buffer loads: a scalar resource per matrix plus a
-  // 32-bit per-lane byte offset (each matrix buffer stays below 2^31 bytes).
   const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(g.a + mat * g.stride_a), 0, 0x7fffffff, kBufferFlags);
   const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(g.b + mat * g.stride_b), 0, 0x7fffffff, kBufferFlags);
   const int lda = static_cast<int>(g.lda), ldb = static_cast<int>(g.ldb);
+  const int rowA0 = ti * 256;
+  const int rowB0 = tj * 256;  // NT: operand-B rows; NN: output columns
 
-  u32x4 ra[8], rb[8];
-  // NT operand slab: thread t loads rows t/8 + 32 i at k-chunk 8 (t % 8).
-  // NN operand slab (K x N): lane loads k rows 8 kb .. 8 kb + 7 at n-chunk nb.
-  const int kb = lane & 7, nb = (lane >> 3) + 8 * wave;
-  const int va = 2 * ((ti * BM + (t >> 3)) * lda + (t & 7) * 8);
-  const int vb = kNN ? 2 * ((kb * 8) * ldb + tj * BN + nb * 8) : 2 * ((tj * BN + (t >> 3)) * ldb + (t & 7) * 8);
+  // ---- global -> LDS slab loads: 8 instructions per wave per operand.
+  // NT: instruction I = 8 wave + i covers rows 8I .. 8I + 7; lane -> row 8I + lane/8, slot lane%8.
+  const int nt_r = lane >> 3;
+  const int nt_c = (lane & 7) ^ nt_r;
+  const int vA = 2 * ((rowA0 + nt_r) * lda + 8 * nt_c);
+  const int vB_nt = 2 * ((rowB0 + nt_r) * ldb + 8 * nt_c);
+  // NN: instruction I = 8 wave + i covers k rows 2I, 2I + 1; lane -> row 2I + lane/32, slot lane%32.
+  const int nn_r = lane >> 5;
+  const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (2 * (nn_r & 3))));
+  const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (2 * ((2 + nn_r) & 3))));
 
-  auto load = [&](int kt) {
+  auto issue_slab = [&](lds_u8* buf, int kt) {
     const int k0 = kt * BK;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) ra[i] = __builtin_amdgcn_raw_buffer_load_b128(rA, va, 2 * (32 * i * lda + k0), 0);
+    for (int i = 0; i < 8; ++i) {
+      const int I = 8 * wave + i;
+      dma16(rA, buf + I * 1024, vA, 2 * (8 * I * lda + k0));
+    }
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      rb[i] = __builtin_amdgcn_raw_buffer_load_b128(rB, vb, kNN ? 2 * ((k0 + i) * ldb) : 2 * (32 * i * ldb + k0), 0);
+    for (int i = 0; i < 8; ++i) {
+      const int I = 8 * wave + i;
+      if (kNN)
+        dma16(rB, buf + 32768 + I * 1024, (i & 1) ? vB_nn1 : vB_nn0, 2 * ((k0 + 2 * I) * ldb));
+      else
+        dma16(rB, buf + 32768 + I * 1024, vB_nt, 2 * (8 * I * ldb + k0));
+    }
   };
 
-  auto store = [&](int buf) {
-    uint16_t* As = lds[buf][0];
-    uint16_t* Bs = lds[buf][1];
+  // ---- fragment addresses (bytes within a buffer)
+  // NT fragment: row R = base + 32 i + lane%32, k chunk 2 kk + lane/32, stored at that chunk ^ (R & 7).
+  const int offA = (wm * 128 + (lane & 31)) * 128;
+  const int offB_nt = 32768 + (wn * 128 + (lane & 31)) * 128;
+  int slot_kk[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      *reinterpret_cast<u32x4*>(As + ((t >> 3) + 32 * i) * PK + (t & 7) * 8) = ra[i];
-    if (kNN) {
-      // 8 x 8 transpose of 16-bit elements: out[c] = column c of the 8 loaded rows.
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const uint32_t sel = (c & 1) ? 0x07060302u : 0x05040100u;
-        const int q = c >> 1;
-        u32x4 o;
-        o.x = __builtin_amdgcn_perm(dword(rb[1], q), dword(rb[0], q), sel);
-        o.y = __builtin_amdgcn_perm(dword(rb[3], q), dword(rb[2], q), sel);
-        o.z = __builtin_amdgcn_perm(dword(rb[5], q), dword(rb[4], q), sel);
-        o.w = __builtin_amdgcn_perm(dword(rb[7], q), dword(rb[6], q), sel);
-        *reinterpret_cast<u32x4*>(Bs + (nb * 8 + c) * PK + kb * 8) = o;
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        *reinterpret_cast<u32x4*>(Bs + ((t >> 3) + 32 * i) * PK + (t & 7) * 8) = rb[i];
-    }
+  for (int kk = 0; kk < 4; ++kk) slot_kk[kk] = 16 * ((2 * kk + h) ^ (lane & 7));
+  // NN fragment via ds_read_b64_tr_b16: within each 16-lane group, lane q points at
+  // k row q / 4 and n columns 4 (q % 4) .. +3; afterwards lane q holds 4 consecutive k
+  // of column q, so two reads give the 8 k values an MFMA operand lane needs.
+  const int jq = lane & 15, grp = lane >> 4;
+  const int nn_k = 8 * (grp >> 1) + (jq >> 2);                // + 16 kk + 4 t
+  const int nn_n = wn * 128 + 16 * (grp & 1) + 4 * (jq & 3);  // + 32 j
+  const int nn_swz = 2 * (nn_k & 3);
+  auto nn_addr = [&](int kk, int t4, int j) {
+    const int k = 16 * kk + nn_k + 4 * t4;
+    const int n = nn_n + 32 * j;
+    return 32768 + k * 512 + 16 * ((n >> 3) ^ nn_swz) + 2 * (n & 7);
   };
 
   floatx16 acc[4][4];
@@ -144,78 +174,169 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // MFMAs of one 16-deep k step use fragments loaded one step earlier, so LDS
-  // latency hides behind the 16 MFMAs of the previous step.
-  auto compute = [&](int buf) {
-    const uint16_t* As = lds[buf][0] + (wm * 128 + (lane & 31)) * PK + (lane >> 5) * 8;
-    const uint16_t* Bs = lds[buf][1] + (wn * 128 + (lane & 31)) * PK + (lane >> 5) * 8;
-    bf16x8 af[2][4], bf[2][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) af[0][i] = *reinterpret_cast<const bf16x8*>(As + i * 32 * PK);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) bf[0][j] = *reinterpret_cast<const bf16x8*>(Bs + j * 32 * PK);
+  auto compute = [&](const lds_u8* buf) {
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      const int cur = kk & 1;
-      if (kk + 1 < BK / 16) {
+      bf16x8 af[4], bfr[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          af[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(As + i * 32 * PK + (kk + 1) * 16);
+      for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(buf + offA + i * 4096 + slot_kk[kk]);
+      if (kNN) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + nn_addr(kk, 0, j)));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + nn_addr(kk, 1, j)));
+          const i16x8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          bfr[j] = __builtin_bit_cast(bf16x8, both);
+        }
+      } else {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          bf[cur ^ 1][j] = *reinterpret_cast<const bf16x8*>(Bs + j * 32 * PK + (kk + 1) * 16);
+          bfr[j] = *reinterpret_cast<const lds_bf16x8*>(buf + offB_nt + j * 4096 + slot_kk[kk]);
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bf[cur][j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < 4; ++j) {
+          // apply: operands swapped so each lane ends up with 4 consecutive output columns
+          if (kNN)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        }
     }
   };
 
+  // ---- main loop: two slabs per trip so that each buffer is its own LDS object.
+  // K is a multiple of 256 (zero padding), so the slab count is even.
   const int nk = g.K / BK;
-  load(0);
-  store(0);
+  issue_slab(lds0, 0);
+  wait_vm();
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load(kt + 1);
-    compute(cur);
-    if (kt + 1 < nk) store(cur ^ 1);
+  for (int kt = 0; kt < nk; kt += 2) {
+    issue_slab(lds1, kt + 1);
+    compute(lds0);
+    wait_vm();
+    __syncthreads();
+    if (kt + 2 < nk) issue_slab(lds0, kt + 2);
+    compute(lds1);
+    wait_vm();
     __syncthreads();
   }
 
-  // Epilogue: C = s * (alpha_e * E + alpha_acc * acc), bf16 round-to-nearest-even.
+  // ---- epilogue.  OUT is the 256 x 256 tile written with whole-row stores:
+  //   apply:     OUT = C(ti, tj); lane holds OUT[128 wm + 32 i + lane%32][128 wn + 32 j + 8 (v/4) + 4 (lane/32) + v%4]
+  //   Gram/poly: OUT = C(tj, ti) = C(ti, tj)^T; lane holds OUT[128 wn + 32 j + lane%32][128 wm + 32 i + ...]
+  // OUT rows 0..127 are staged in lds0, rows 128..255 in lds1.
+  const int out_row0 = kNN ? rowA0 : rowB0;
+  const int out_col0 = kNN ? rowB0 : rowA0;
   float s = 1.f;
   if (g.scale_kind != 0) s = g.fold[2 * mat + (g.scale_kind - 1)];
   const float ae = g.alpha_e * s, aa = g.alpha_acc * s;
-  uint16_t* __restrict__ C = g.c + mat * g.stride_c;
-  const uint16_t* __restrict__ E = kHasE ? g.e + mat * g.stride_e : nullptr;
-  const bool mirror = kSym && ti != tj;
+  const int own_half = kNN ? wm : wn;  // staged half holding this wave's OUT rows
+  const int own_col = kNN ? wn : wm;   // 128-column half holding this wave's OUT columns
+  lds_u8* stage = own_half ? lds1 : lds0;
+  const int ldo = static_cast<int>(g.ldc);
+
+  if (kHasE) {
+    // stage E (the same rows and columns as OUT): per half 64 instructions, 16 per wave
+    const __amdgpu_buffer_rsrc_t rE = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(g.e + mat * g.stride_e), 0, 0x7fffffff, kBufferFlags);
+    const int lde = static_cast<int>(g.lde);
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      lds_u8* dst = half ? lds1 : lds0;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int I = 16 * wave + i;  // rows 2I, 2I + 1 of this half
+        const int rr = 2 * I + h;
+        const int c = (lane & 31) ^ (rr & 31);
+        dma16(rE, dst + I * 1024, 2 * ((out_row0 + 128 * half + h) * lde + out_col0 + 8 * c), 2 * (2 * I * lde));
+      }
+    }
+    wait_vm();
+    __syncthreads();
+  }
+
+  // combine: each lane owns 4 consecutive OUT columns per (i, j, v/4).  All staged E reads
+  // come before any staged write so that they can all be in flight at once.
+  u32x2 packed[4][4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int col = tj * BN + wn * 128 + j * 32 + (lane & 31);
+      const int rr = 32 * (kNN ? i : j) + (lane & 31);
 #pragma unroll
-      for (int vb = 0; vb < 4; ++vb) {
-        const int row0 = ti * BM + wm * 128 + i * 32 + vb * 8 + (lane >> 5) * 4;
-        uint16_t h[4];
+      for (int vq = 0; vq < 4; ++vq) {
+        const int c = 128 * own_col + 32 * (kNN ? j : i) + 8 * vq + 4 * h;
+        float o[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int row = row0 + v;
-          float val = aa * acc[i][j][vb * 4 + v];
-          if (kHasE) val = fmaf(ae, bf16_to_f32(E[static_cast<int64_t>(row) * g.lde + col]), val);
-          h[v] = f32_to_bf16(val);
-          C[static_cast<int64_t>(row) * g.ldc + col] = h[v];
+        for (int q = 0; q < 4; ++q) o[q] = aa * acc[i][j][4 * vq + q];
+        if (kHasE) {
+          const u32x2 e = *reinterpret_cast<const lds_u32x2*>(stage + stage_byte(rr, c));
+          o[0] = fmaf(ae, bf16_to_f32(e.x & 0xffffu), o[0]);
+          o[1] = fmaf(ae, bf16_to_f32(e.x >> 16), o[1]);
+          o[2] = fmaf(ae, bf16_to_f32(e.y & 0xffffu), o[2]);
+          o[3] = fmaf(ae, bf16_to_f32(e.y >> 16), o[3]);
         }
-        if (mirror) {
-          u32x2 pk;
-          pk.x = h[0] | (static_cast<uint32_t>(h[1]) << 16);
-          pk.y = h[2] | (static_cast<uint32_t>(h[3]) << 16);
-          *reinterpret_cast<u32x2*>(C + static_cast<int64_t>(col) * g.ldc + row0) = pk;
-        }
+        packed[i][j][vq].x = pack_bf16x2(o[0], o[1]);
+        packed[i][j][vq].y = pack_bf16x2(o[2], o[3]);
       }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int rr = 32 * (kNN ? i : j) + (lane & 31);
+#pragma unroll
+      for (int vq = 0; vq < 4; ++vq) {
+        const int c = 128 * own_col + 32 * (kNN ? j : i) + 8 * vq + 4 * h;
+        *reinterpret_cast<lds_u32x2*>(stage + stage_byte(rr, c)) = packed[i][j][vq];
+      }
+    }
+  __syncthreads();
+
+  // whole-row stores of OUT: each wave instruction writes 2 full rows
+  uint16_t* __restrict__ C = g.c + mat * g.stride_c;
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    const lds_u8* src = half ? lds1 : lds0;
+#pragma unroll 4
+    for (int it = 0; it < 16; ++it) {
+      const int q = it * 256 + t;
+      const int rr = q >> 5, p = q & 31;
+      const u32x4 v = *reinterpret_cast<const lds_u32x4*>(src + rr * 512 + 16 * p);
+      const int c = p ^ (rr & 31);
+      *reinterpret_cast<u32x4*>(C + static_cast<int64_t>(out_row0 + 128 * half + rr) * ldo + out_col0 + 8 * c) = v;
+    }
+  }
+
+  if (kSym && ti != tj) {
+    // Mirrored tile C(ti, tj) = OUT^T.  Transpose reads give each lane 4 consecutive OUT rows
+    // of one OUT column (= 4 consecutive columns of one C(ti, tj) row); two reads make 16
+    // bytes.  Per trip a 16-lane group covers 16 OUT columns x 8 OUT rows and the 4 groups
+    // of a wave take consecutive 8-row blocks, so a wave writes 64 contiguous bytes in each
+    // of 16 rows.
+    const int jq16 = lane & 15, g4 = lane >> 4;
+#pragma unroll 2
+    for (int it = 0; it < 32; ++it) {
+      const int blk = it * 4 + wave;           // 128 blocks: 16 column blocks x 8 row blocks
+      const int cb = blk & 15, rb = blk >> 4;
+      const int r0 = 32 * rb + 8 * g4;         // OUT rows r0 .. r0 + 7
+      const int c0 = 16 * cb;
+      const lds_u8* src = (r0 >= 128) ? lds1 : lds0;
+      u32x4 out;
+#pragma unroll
+      for (int t4 = 0; t4 < 2; ++t4) {
+        const int rr = (r0 & 127) + 4 * t4 + (jq16 >> 2);
+        const int c = c0 + 4 * (jq16 & 3);
+        const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(src + stage_byte(rr, c)));
+        const u32x2 w = __builtin_bit_cast(u32x2, v);
+        out[2 * t4] = w.x;
+        out[2 * t4 + 1] = w.y;
+      }
+      // lane holds OUT[r0 .. r0 + 7][c0 + jq16] = C(ti, tj)[c0 + jq16][r0 .. r0 + 7]
+      *reinterpret_cast<u32x4*>(C + static_cast<int64_t>(rowA0 + c0 + jq16) * ldo + rowB0 + r0) = out;
     }
   }
 }
