@@ -21,10 +21,9 @@ ARCH = "gfx950"
 # Packed-fp32 VALU forms are disabled for all device code (plain float code only).
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", f"-I{INCLUDE}", f"-I{CSRC}",
           "-fvisibility=hidden", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-# Per-source extra flags.  The MFMA GEMM uses the iterative ILP scheduler, which
-# keeps a whole 16-deep k step's LDS fragments in flight ahead of its MFMAs.
+# Per-source extra flags.
 SOURCES = {
-    "k_ns_gemm.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
+    "k_ns_gemm.hip": [],
     "k_stream.hip": [],
     "meq_api.cpp": [],
 }

@@ -7,12 +7,13 @@
 //
 // One workgroup = 4 waves = one 256 x 256 output tile; each wave owns a 128 x 128
 // quadrant as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation in AGPRs).
-// K advances in slabs of 64.  Global -> LDS traffic uses buffer loads that write
-// LDS directly (no registers, no LDS store instructions), double-buffered, with
-// 16-byte chunks XOR-swizzled so that fragment reads are bank-conflict free.
-// The epilogue stages the output tile (and the tile it adds, X or A) in LDS and
-// writes whole rows with 16-byte stores.  Same-shape matrices form one launch;
-// workgroup ids are remapped so each XCD receives a contiguous run of tiles.
+// K advances in slabs of 32 through a 4-stage LDS ring (three slabs in flight while
+// one is consumed, which covers the latency of the loads that miss L2).  Global ->
+// LDS traffic uses buffer loads that write LDS directly (no registers, no LDS store
+// instructions); 16-byte chunks are XOR-swizzled so fragment reads are free of bank
+// conflicts.  The epilogue stages the output tile (and the tile it adds, X or A) in
+// LDS and writes whole rows with 16-byte stores.  Same-shape matrices form one
+// launch; workgroup ids are remapped so each XCD receives a contiguous run of tiles.
 #include "meq_internal.h"
 
 namespace meq {
@@ -20,8 +21,8 @@ namespace meq {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -32,14 +33,13 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
-constexpr int BK = 64;
-constexpr int kBufBytes = 65536;  // one LDS buffer: operand A slab (32 KiB) + operand B slab (32 KiB)
+constexpr int BK = 32;              // k per slab
+constexpr int kStageBytes = 32768;  // one ring stage: operand A slab (16 KiB) + operand B slab (16 KiB)
+constexpr int kDmaPerSlab = 8;      // LDS-bound buffer loads per wave per slab (4 per operand)
 // Buffer resource word 3 for raw (untyped, 32-bit format) buffer access on gfx9.
 constexpr int kBufferFlags = 0x00020000;
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
-
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Two floats -> packed bf16 pair (v_cvt_pk_bf16_f32: round to nearest even), lo first.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -61,24 +61,60 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, lds_u8* dst, in
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)dst, 16, voff, soff, 0, 0);
 }
 
-// s_waitcnt vmcnt(0) (expcnt and lgkmcnt left at their maxima).
-__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+// s_waitcnt vmcnt(n) with expcnt and lgkmcnt left at their maxima (gfx9 encoding).
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | 0x0f70);
+}
 
-// LDS layouts (bytes):
-//   NT slab (256 rows x 64 k):  row r at r * 128; 16-byte chunk c (k = 8c..8c+7) at slot c ^ (r & 7).
-//   NN slab (64 k x 256 n):     row k at k * 512; chunk c (n = 8c..8c+7) at slot c ^ (2 (k & 3)).
-//   staged output half (128 x 256): row r at r * 512; chunk c at slot c ^ (r & 31).
-__device__ __forceinline__ int stage_byte(int rr, int c) { return rr * 512 + 16 * ((c >> 3) ^ (rr & 31)) + 2 * (c & 7); }
+// LDS layouts (bytes).  Each 16-lane pass of an LDS access covers 256 bytes (64 banks).
+//   NT slab (256 rows x 32 k):   row r at r * 64; 16-byte chunk c (k = 8c..8c+7) at slot c ^ ((r >> 2) & 3),
+//                                so 16 consecutive rows read at one chunk fill the 256 bytes exactly.
+//   NN slab (32 k x 256 n):      row k at k * 512; chunk c (n = 8c..8c+7) at slot c ^ (2 (k & 3)).
+//   staged output (256 x 256):   row r in ring stage r / 64 at (r % 64) * 512; chunk c at slot c ^ (r & 31).
+__device__ __forceinline__ int stage_byte(int rr, int c) {
+  return (rr & 63) * 512 + 16 * ((c >> 3) ^ (rr & 31)) + 2 * (c & 7);
+}
+
+// Scheduling pattern of one 16-MFMA k step: kReads LDS reads (for the next step) and
+// kDma LDS-bound buffer loads interleaved between the MFMAs.
+template <int kReads, int kDma>
+__device__ __forceinline__ void sched_step() {
+#ifndef MEQ_NO_SCHED
+#define MEQ_SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
+#define MEQ_QUAD(r, d)          \
+  if (r > 0) MEQ_SG(0x100, r);  \
+  MEQ_SG(0x008, 1);             \
+  if (d > 0) MEQ_SG(0x020, d);  \
+  MEQ_SG(0x008, 1);             \
+  if (r > 0) MEQ_SG(0x100, r);  \
+  MEQ_SG(0x008, 1);             \
+  MEQ_SG(0x008, 1);
+  constexpr int r0 = kReads / 8, r1 = kReads / 4 - kReads / 8;  // 4 (r0 + r1) reads
+  constexpr int d = kDma / 4;
+  MEQ_QUAD(r1, d) MEQ_QUAD(r0, d) MEQ_QUAD(r1, d) MEQ_QUAD(r0, d)
+#undef MEQ_QUAD
+#undef MEQ_SG
+#endif
+}
 
 template <int kMode>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_ns_gemm(GemmArgs g) {
   constexpr bool kNN = kMode == 2;
   constexpr bool kSym = kMode != 2;
   constexpr bool kHasE = kMode != 0;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds0_[kBufBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t lds1_[kBufBytes];
-  lds_u8* const lds0 = (lds_u8*)lds0_;
-  lds_u8* const lds1 = (lds_u8*)lds1_;
+  // Four ring stages as separate objects, so the compiler can tell the stage being read
+  // from the stages being filled.
+  __shared__ __attribute__((aligned(1024))) uint8_t st0_[kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st1_[kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st2_[kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st3_[kStageBytes];
+  lds_u8* const st0 = (lds_u8*)st0_;
+  lds_u8* const st1 = (lds_u8*)st1_;
+  lds_u8* const st2 = (lds_u8*)st2_;
+  lds_u8* const st3 = (lds_u8*)st3_;
+  auto stage_of = [&](int q) { return q == 0 ? st0 : q == 1 ? st1 : q == 2 ? st2 : st3; };
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -118,13 +154,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int rowA0 = ti * 256;
   const int rowB0 = tj * 256;  // NT: operand-B rows; NN: output columns
 
-  // ---- global -> LDS slab loads: 8 instructions per wave per operand.
-  // NT: instruction I = 8 wave + i covers rows 8I .. 8I + 7; lane -> row 8I + lane/8, slot lane%8.
-  const int nt_r = lane >> 3;
-  const int nt_c = (lane & 7) ^ nt_r;
+  // ---- global -> LDS slab loads: 4 instructions per wave per operand (1 KiB each).
+  // NT: instruction I = 4 wave + i covers rows 16I .. 16I + 15; lane -> row 16I + lane/4,
+  //     slot lane%4, which holds chunk slot ^ ((row >> 2) & 3) = slot ^ (lane >> 4).
+  const int nt_r = lane >> 2;
+  const int nt_c = (lane & 3) ^ (lane >> 4);
   const int vA = 2 * ((rowA0 + nt_r) * lda + 8 * nt_c);
   const int vB_nt = 2 * ((rowB0 + nt_r) * ldb + 8 * nt_c);
-  // NN: instruction I = 8 wave + i covers k rows 2I, 2I + 1; lane -> row 2I + lane/32, slot lane%32.
+  // NN: instruction I = 4 wave + i covers k rows 2I, 2I + 1; lane -> row 2I + lane/32, slot lane%32.
   const int nn_r = lane >> 5;
   const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (2 * (nn_r & 3))));
   const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (2 * ((2 + nn_r) & 3))));
@@ -132,27 +169,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   auto issue_slab = [&](lds_u8* buf, int kt) {
     const int k0 = kt * BK;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int I = 8 * wave + i;
-      dma16(rA, buf + I * 1024, vA, 2 * (8 * I * lda + k0));
+    for (int i = 0; i < 4; ++i) {
+      const int I = 4 * wave + i;
+      dma16(rA, buf + I * 1024, vA, 2 * (16 * I * lda + k0));
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int I = 8 * wave + i;
+    for (int i = 0; i < 4; ++i) {
+      const int I = 4 * wave + i;
       if (kNN)
-        dma16(rB, buf + 32768 + I * 1024, (i & 1) ? vB_nn1 : vB_nn0, 2 * ((k0 + 2 * I) * ldb));
+        dma16(rB, buf + 16384 + I * 1024, (i & 1) ? vB_nn1 : vB_nn0, 2 * ((k0 + 2 * I) * ldb));
       else
-        dma16(rB, buf + 32768 + I * 1024, vB_nt, 2 * (8 * I * ldb + k0));
+        dma16(rB, buf + 16384 + I * 1024, vB_nt, 2 * (16 * I * ldb + k0));
     }
   };
 
-  // ---- fragment addresses (bytes within a buffer)
-  // NT fragment: row R = base + 32 i + lane%32, k chunk 2 kk + lane/32, stored at that chunk ^ (R & 7).
-  const int offA = (wm * 128 + (lane & 31)) * 128;
-  const int offB_nt = 32768 + (wn * 128 + (lane & 31)) * 128;
-  int slot_kk[4];
+  // ---- fragment addresses (bytes within a stage)
+  // NT fragment: row R = base + 32 i + lane%32 (base a multiple of 32), k chunk 2 kk + lane/32,
+  // at slot chunk ^ ((R >> 2) & 3) = chunk ^ ((lane >> 2) & 3).
+  const int offA = (wm * 128 + (lane & 31)) * 64;
+  const int offB_nt = 16384 + (wn * 128 + (lane & 31)) * 64;
+  int slot_kk[2];
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) slot_kk[kk] = 16 * ((2 * kk + h) ^ (lane & 7));
+  for (int kk = 0; kk < 2; ++kk) slot_kk[kk] = 16 * ((2 * kk + h) ^ ((lane >> 2) & 3));
   // NN fragment via ds_read_b64_tr_b16: within each 16-lane group, lane q points at
   // k row q / 4 and n columns 4 (q % 4) .. +3; afterwards lane q holds 4 consecutive k
   // of column q, so two reads give the 8 k values an MFMA operand lane needs.
@@ -163,7 +201,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   auto nn_addr = [&](int kk, int t4, int j) {
     const int k = 16 * kk + nn_k + 4 * t4;
     const int n = nn_n + 32 * j;
-    return 32768 + k * 512 + 16 * ((n >> 3) ^ nn_swz) + 2 * (n & 7);
+    return 16384 + k * 512 + 16 * ((n >> 3) ^ nn_swz) + 2 * (n & 7);
   };
 
   floatx16 acc[4][4];
@@ -174,86 +212,112 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  auto compute = [&](const lds_u8* buf) {
+  auto load_frags = [&](const lds_u8* buf, int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[4]) {
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 af[4], bfr[4];
+    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(buf + offA + i * 2048 + slot_kk[kk]);
+    if (kNN) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(buf + offA + i * 4096 + slot_kk[kk]);
-      if (kNN) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + nn_addr(kk, 0, j)));
-          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + nn_addr(kk, 1, j)));
-          const i16x8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          bfr[j] = __builtin_bit_cast(bf16x8, both);
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          bfr[j] = *reinterpret_cast<const lds_bf16x8*>(buf + offB_nt + j * 4096 + slot_kk[kk]);
+      for (int j = 0; j < 4; ++j) {
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + nn_addr(kk, 0, j)));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + nn_addr(kk, 1, j)));
+        bfr[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
+    } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          // apply: operands swapped so each lane ends up with 4 consecutive output columns
-          if (kNN)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
-          else
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-        }
+      for (int j = 0; j < 4; ++j)
+        bfr[j] = *reinterpret_cast<const lds_bf16x8*>(buf + offB_nt + j * 2048 + slot_kk[kk]);
     }
   };
 
-  // ---- main loop: two slabs per trip so that each buffer is its own LDS object.
-  // K is a multiple of 256 (zero padding), so the slab count is even.
+  auto mfma16 = [&](const bf16x8 (&af)[4], const bf16x8 (&bfr)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        // apply: operands swapped so each lane ends up with 4 consecutive output columns
+        if (kNN)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+        else
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      }
+  };
+
+  // Software pipeline over slabs (slab s lives in ring stage s % 4).  On entry to
+  // slab kt its first k step's fragments are already in registers (fa).  The wave reads
+  // the second step's fragments under the first step's MFMAs, then waits for its own
+  // loads of slab kt + 1 and meets the other waves: slab kt + 1 has fully landed and no
+  // wave reads slab kt's stage any more, so that stage is refilled with slab kt + 4 and
+  // slab kt + 1's first fragments are read under the second step's MFMAs.
   const int nk = g.K / BK;
-  issue_slab(lds0, 0);
-  wait_vm();
-  __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    issue_slab(lds1, kt + 1);
-    compute(lds0);
-    wait_vm();
-    __syncthreads();
-    if (kt + 2 < nk) issue_slab(lds0, kt + 2);
-    compute(lds1);
-    wait_vm();
-    __syncthreads();
+  bf16x8 fa[4], fb[4], ga[4], gb[4];
+  auto bar = [] {
+    // A bare barrier: __syncthreads() would also wait for the newer slabs' loads.  The
+    // empty asm statements keep the compiler from moving memory accesses across it.
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  auto slab = [&](lds_u8* cur, const lds_u8* nxt, int kt) {
+    load_frags(cur, 1, ga, gb);
+    mfma16(fa, fb);
+    sched_step<kNN ? 12 : 8, 0>();
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave is done reading slab kt
+    wait_vm<2 * kDmaPerSlab>();          // this wave's loads of slab kt + 1 have landed
+    bar();
+    issue_slab(cur, min(kt + 4, nk - 1));  // past the end: a harmless reload of the last slab
+    load_frags(nxt, 0, fa, fb);
+    mfma16(ga, gb);
+    sched_step<kNN ? 12 : 8, kDmaPerSlab>();
+  };
+
+  // ---- main loop: four slabs per trip so every stage is addressed statically.
+  // K is a multiple of 256 (zero padding), so the slab count is a multiple of 8.
+  issue_slab(st0, 0);
+  issue_slab(st1, 1);
+  issue_slab(st2, 2);
+  issue_slab(st3, 3);
+  wait_vm<3 * kDmaPerSlab>();
+  bar();
+  load_frags(st0, 0, fa, fb);
+  for (int kt = 0; kt < nk; kt += 4) {
+    slab(st0, st1, kt);
+    slab(st1, st2, kt + 1);
+    slab(st2, st3, kt + 2);
+    slab(st3, st0, kt + 3);
   }
+  wait_vm<0>();
+  __syncthreads();
 
   // ---- epilogue.  OUT is the 256 x 256 tile written with whole-row stores:
   //   apply:     OUT = C(ti, tj); lane holds OUT[128 wm + 32 i + lane%32][128 wn + 32 j + 8 (v/4) + 4 (lane/32) + v%4]
   //   Gram/poly: OUT = C(tj, ti) = C(ti, tj)^T; lane holds OUT[128 wn + 32 j + lane%32][128 wm + 32 i + ...]
-  // OUT rows 0..127 are staged in lds0, rows 128..255 in lds1.
+  // OUT row r is staged in ring stage r / 64.
   const int out_row0 = kNN ? rowA0 : rowB0;
   const int out_col0 = kNN ? rowB0 : rowA0;
   float s = 1.f;
   if (g.scale_kind != 0) s = g.fold[2 * mat + (g.scale_kind - 1)];
   const float ae = g.alpha_e * s, aa = g.alpha_acc * s;
-  const int own_half = kNN ? wm : wn;  // staged half holding this wave's OUT rows
-  const int own_col = kNN ? wn : wm;   // 128-column half holding this wave's OUT columns
-  lds_u8* stage = own_half ? lds1 : lds0;
+  const int own_row = kNN ? wm : wn;  // 128-row half holding this wave's OUT rows
+  const int own_col = kNN ? wn : wm;  // 128-column half holding this wave's OUT columns
   const int ldo = static_cast<int>(g.ldc);
 
   if (kHasE) {
-    // stage E (the same rows and columns as OUT): per half 64 instructions, 16 per wave
+    // stage E (the same rows and columns as OUT): 32 instructions per stage, 2 rows each
     const __amdgpu_buffer_rsrc_t rE = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(g.e + mat * g.stride_e), 0, 0x7fffffff, kBufferFlags);
     const int lde = static_cast<int>(g.lde);
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      lds_u8* dst = half ? lds1 : lds0;
+    for (int q = 0; q < 4; ++q) {
+      lds_u8* dst = stage_of(q);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int I = 16 * wave + i;  // rows 2I, 2I + 1 of this half
-        const int rr = 2 * I + h;
-        const int c = (lane & 31) ^ (rr & 31);
-        dma16(rE, dst + I * 1024, 2 * ((out_row0 + 128 * half + h) * lde + out_col0 + 8 * c), 2 * (2 * I * lde));
+      for (int i = 0; i < 8; ++i) {
+        const int I = 8 * wave + i;  // rows 2I, 2I + 1 of this stage
+        const int r = 64 * q + 2 * I + h;
+        const int c = (lane & 31) ^ (r & 31);
+        dma16(rE, dst + I * 1024, 2 * ((out_row0 + 64 * q + h) * lde + out_col0 + 8 * c), 2 * (2 * I * lde));
       }
     }
-    wait_vm();
+    wait_vm<0>();
     __syncthreads();
   }
 
@@ -264,7 +328,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int rr = 32 * (kNN ? i : j) + (lane & 31);
+      const int r = 128 * own_row + 32 * (kNN ? i : j) + (lane & 31);
+      const lds_u8* src = stage_of(2 * own_row + ((kNN ? i : j) >> 1));
 #pragma unroll
       for (int vq = 0; vq < 4; ++vq) {
         const int c = 128 * own_col + 32 * (kNN ? j : i) + 8 * vq + 4 * h;
@@ -272,7 +337,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
         for (int q = 0; q < 4; ++q) o[q] = aa * acc[i][j][4 * vq + q];
         if (kHasE) {
-          const u32x2 e = *reinterpret_cast<const lds_u32x2*>(stage + stage_byte(rr, c));
+          const u32x2 e = *reinterpret_cast<const lds_u32x2*>(src + stage_byte(r, c));
           o[0] = fmaf(ae, bf16_to_f32(e.x & 0xffffu), o[0]);
           o[1] = fmaf(ae, bf16_to_f32(e.x >> 16), o[1]);
           o[2] = fmaf(ae, bf16_to_f32(e.y & 0xffffu), o[2]);
@@ -287,11 +352,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int rr = 32 * (kNN ? i : j) + (lane & 31);
+      const int r = 128 * own_row + 32 * (kNN ? i : j) + (lane & 31);
+      lds_u8* dst = stage_of(2 * own_row + ((kNN ? i : j) >> 1));
 #pragma unroll
       for (int vq = 0; vq < 4; ++vq) {
         const int c = 128 * own_col + 32 * (kNN ? j : i) + 8 * vq + 4 * h;
-        *reinterpret_cast<lds_u32x2*>(stage + stage_byte(rr, c)) = packed[i][j][vq];
+        *reinterpret_cast<lds_u32x2*>(dst + stage_byte(r, c)) = packed[i][j][vq];
       }
     }
   __syncthreads();
@@ -299,15 +365,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // whole-row stores of OUT: each wave instruction writes 2 full rows
   uint16_t* __restrict__ C = g.c + mat * g.stride_c;
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    const lds_u8* src = half ? lds1 : lds0;
-#pragma unroll 4
-    for (int it = 0; it < 16; ++it) {
-      const int q = it * 256 + t;
-      const int rr = q >> 5, p = q & 31;
+  for (int q = 0; q < 4; ++q) {
+    const lds_u8* src = stage_of(q);
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+      const int idx = it * 256 + t;
+      const int rr = idx >> 5, p = idx & 31;  // row within the stage, slot
       const u32x4 v = *reinterpret_cast<const lds_u32x4*>(src + rr * 512 + 16 * p);
-      const int c = p ^ (rr & 31);
-      *reinterpret_cast<u32x4*>(C + static_cast<int64_t>(out_row0 + 128 * half + rr) * ldo + out_col0 + 8 * c) = v;
+      const int r = 64 * q + rr;
+      const int c = p ^ (r & 31);
+      *reinterpret_cast<u32x4*>(C + static_cast<int64_t>(out_row0 + r) * ldo + out_col0 + 8 * c) = v;
     }
   }
 
@@ -320,17 +387,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int jq16 = lane & 15, g4 = lane >> 4;
 #pragma unroll 2
     for (int it = 0; it < 32; ++it) {
-      const int blk = it * 4 + wave;           // 128 blocks: 16 column blocks x 8 row blocks
+      const int blk = it * 4 + wave;  // 128 blocks: 16 column blocks x 8 row blocks
       const int cb = blk & 15, rb = blk >> 4;
-      const int r0 = 32 * rb + 8 * g4;         // OUT rows r0 .. r0 + 7
+      const int r0 = 32 * rb + 8 * g4;  // OUT rows r0 .. r0 + 7 (one stage)
       const int c0 = 16 * cb;
-      const lds_u8* src = (r0 >= 128) ? lds1 : lds0;
+      const lds_u8* src = r0 < 64 ? st0 : r0 < 128 ? st1 : r0 < 192 ? st2 : st3;
       u32x4 out;
 #pragma unroll
       for (int t4 = 0; t4 < 2; ++t4) {
-        const int rr = (r0 & 127) + 4 * t4 + (jq16 >> 2);
+        const int r = r0 + 4 * t4 + (jq16 >> 2);
         const int c = c0 + 4 * (jq16 & 3);
-        const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(src + stage_byte(rr, c)));
+        const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(src + stage_byte(r, c)));
         const u32x2 w = __builtin_bit_cast(u32x2, v);
         out[2 * t4] = w.x;
         out[2 * t4 + 1] = w.y;

@@ -137,8 +137,8 @@ class Plan:
 
     def __del__(self):
         h = getattr(self, "_h", None)
-        if h is not None and h.value:
-            lib().meq_destroy(h)
+        if h is not None and h.value and _lib is not None:
+            _lib.meq_destroy(h)
             self._h = None
 
     @property
