@@ -85,6 +85,9 @@ def main() -> int:
     ap.add_argument("--lr", type=float, default=0.02)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=30.0, help="seconds of oracle work at most")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one plain 256 MiB device-to-device copy before the warm-up, as the reference "
+                         "kernel of known size for FETCH_SIZE / WRITE_SIZE counter runs")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the MeqMuon update is measured on a single MI355X; "
@@ -108,7 +111,12 @@ def main() -> int:
     hp = upd.plan.hparams
     print(f"# bench: workspace {upd.plan.workspace_bytes / 2**30:.2f} GiB, groups {upd.plan.groups()}",
           file=sys.stderr, flush=True)
-    stream = torch.cuda.current_stream(dev)
+    if args.copy_calibration:
+        src = torch.ones(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         upd.step(grads, args.lr)
     torch.cuda.synchronize()

@@ -47,8 +47,10 @@ def build(verbose: bool = False) -> str:
             cmd = [cc, *COMMON, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
             if verbose:
                 print(" ".join(cmd), flush=True)
-            subprocess.run(cmd, check=True, stdout=subprocess.PIPE if not verbose else None,
-                           stderr=subprocess.STDOUT if not verbose else None)
+            res = subprocess.run(cmd, stdout=subprocess.PIPE if not verbose else None,
+                                 stderr=subprocess.STDOUT if not verbose else None, text=True)
+            if res.returncode != 0:
+                raise RuntimeError(f"hipcc failed on {src}:\n{res.stdout or ''}")
             objs.append(obj)
         out_tmp = LIB + ".tmp"
         cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", out_tmp]

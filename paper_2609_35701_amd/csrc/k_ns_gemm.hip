@@ -71,7 +71,8 @@ __device__ __forceinline__ void wait_vm() {
 // LDS layouts (bytes).  Each 16-lane pass of an LDS access covers 256 bytes (64 banks).
 //   NT slab (256 rows x 32 k):   row r at r * 64; 16-byte chunk c (k = 8c..8c+7) at slot c ^ ((r >> 2) & 3),
 //                                so 16 consecutive rows read at one chunk fill the 256 bytes exactly.
-//   NN slab (32 k x 256 n):      row k at k * 512; chunk c (n = 8c..8c+7) at slot c ^ (2 (k & 3)).
+//   NN slab (32 k x 256 n):      row k at k * 512; chunk c (n = 8c..8c+7) at slot c ^ (4 (k & 3)), so the
+//                                4 rows x 4 chunks a 32-lane transpose read touches fill 256 bytes exactly.
 //   staged output (256 x 256):   row r in ring stage r / 64 at (r % 64) * 512; chunk c at slot c ^ (r & 31).
 __device__ __forceinline__ int stage_byte(int rr, int c) {
   return (rr & 63) * 512 + 16 * ((c >> 3) ^ (rr & 31)) + 2 * (c & 7);
@@ -100,7 +101,7 @@ __device__ __forceinline__ void sched_step() {
 }
 
 template <int kMode>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_ns_gemm(GemmArgs g) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_ns_gemm(GemmArgs args) {
   constexpr bool kNN = kMode == 2;
   constexpr bool kSym = kMode != 2;
   constexpr bool kHasE = kMode != 0;
@@ -122,7 +123,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int wm = wave >> 1, wn = wave & 1;
   const int h = lane >> 5;
 
-  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  // workgroup -> (shape group, matrix, tile).  Each group's range starts at a multiple
+  // of 8, so the XCD remap runs within the group.
+  int gi = 0;
+  while (gi + 1 < args.count && static_cast<int>(blockIdx.x) >= args.tile_start[gi + 1]) ++gi;
+  const GemmGroup& g = args.grp[gi];
+  const int u = blockIdx.x - args.tile_start[gi];
+  const int logical = xcd_remap(u, args.tile_start[gi + 1] - args.tile_start[gi]);
+  if (logical >= g.tiles) return;  // padding slot (uniform over the workgroup)
   const int mat = logical / g.tiles_per_mat;
   int tile = logical - mat * g.tiles_per_mat;
   int ti, tj;
@@ -150,7 +158,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       const_cast<uint16_t*>(g.a + mat * g.stride_a), 0, 0x7fffffff, kBufferFlags);
   const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(g.b + mat * g.stride_b), 0, 0x7fffffff, kBufferFlags);
-  const int lda = static_cast<int>(g.lda), ldb = static_cast<int>(g.ldb);
+  const int lda = g.lda, ldb = g.ldb;
   const int rowA0 = ti * 256;
   const int rowB0 = tj * 256;  // NT: operand-B rows; NN: output columns
 
@@ -163,8 +171,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int vB_nt = 2 * ((rowB0 + nt_r) * ldb + 8 * nt_c);
   // NN: instruction I = 4 wave + i covers k rows 2I, 2I + 1; lane -> row 2I + lane/32, slot lane%32.
   const int nn_r = lane >> 5;
-  const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (2 * (nn_r & 3))));
-  const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (2 * ((2 + nn_r) & 3))));
+  const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * (nn_r & 3))));
+  const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * ((2 + nn_r) & 3))));
 
   auto issue_slab = [&](lds_u8* buf, int kt) {
     const int k0 = kt * BK;
@@ -197,7 +205,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int jq = lane & 15, grp = lane >> 4;
   const int nn_k = 8 * (grp >> 1) + (jq >> 2);                // + 16 kk + 4 t
   const int nn_n = wn * 128 + 16 * (grp & 1) + 4 * (jq & 3);  // + 32 j
-  const int nn_swz = 2 * (nn_k & 3);
+  const int nn_swz = 4 * (nn_k & 3);
   auto nn_addr = [&](int kk, int t4, int j) {
     const int k = 16 * kk + nn_k + 4 * t4;
     const int n = nn_n + 32 * j;
@@ -295,17 +303,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int out_row0 = kNN ? rowA0 : rowB0;
   const int out_col0 = kNN ? rowB0 : rowA0;
   float s = 1.f;
-  if (g.scale_kind != 0) s = g.fold[2 * mat + (g.scale_kind - 1)];
-  const float ae = g.alpha_e * s, aa = g.alpha_acc * s;
+  if (args.scale_kind != 0) s = g.fold[2 * mat + (args.scale_kind - 1)];
+  const float ae = args.alpha_e * s, aa = args.alpha_acc * s;
   const int own_row = kNN ? wm : wn;  // 128-row half holding this wave's OUT rows
   const int own_col = kNN ? wn : wm;  // 128-column half holding this wave's OUT columns
-  const int ldo = static_cast<int>(g.ldc);
+  const int ldo = g.ldc;
 
   if (kHasE) {
     // stage E (the same rows and columns as OUT): 32 instructions per stage, 2 rows each
     const __amdgpu_buffer_rsrc_t rE = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(g.e + mat * g.stride_e), 0, 0x7fffffff, kBufferFlags);
-    const int lde = static_cast<int>(g.lde);
+    const int lde = g.lde;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       lds_u8* dst = stage_of(q);
@@ -411,7 +419,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, int mode, hipStream_t st) {
-  const int blocks = a.tiles_per_mat * a.batch;
+  const int blocks = a.tile_start[a.count];
   switch (mode) {
     case 0: hipLaunchKernelGGL(k_ns_gemm<0>, dim3(blocks), dim3(256), 0, st, a); break;
     case 1: hipLaunchKernelGGL(k_ns_gemm<1>, dim3(blocks), dim3(256), 0, st, a); break;

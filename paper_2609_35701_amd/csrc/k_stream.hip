@@ -197,10 +197,8 @@ __global__ __launch_bounds__(256) void k_rowcol(RowColArgs a) {
 }
 
 // --------------------------------------------------------------------------------
-// One block per matrix: finish r and c (eq. "row-col-rms") from the tile partials,
-// their CVs over entries above delta (eq. "cv", double, two passes), the direction
-// (rows iff gamma_r >= gamma_c, eq. "hidden") and the scale vector of N_r or N_c
-// (eq. "operators"; entries at or below delta get scale 0).
+// Population standard deviation over mean of the entries above delta (eq. "cv"), two
+// passes with fixed-order block reductions; 0 when no entry is above delta.
 __device__ double cv_of(const double* v, int len, double delta, double* red) {
   double s = 0.0, cnt = 0.0;
   for (int i = threadIdx.x; i < len; i += 256) {
@@ -220,32 +218,38 @@ __device__ double cv_of(const double* v, int len, double delta, double* red) {
   return sqrt(q / cnt) / mean;
 }
 
+// r and c (eq. "row-col-rms") from the tile partials, in double: block (x, y) covers
+// lines 256 x .. 256 x + 255 of matrix y, where lines 0 .. s-1 are the wide rows and
+// s .. s+l-1 the wide columns.  A tall matrix's wide rows are its own columns.
+__global__ __launch_bounds__(256) void k_rms(SelectArgs a) {
+  const int mi = blockIdx.y;
+  const int m = a.m[mi], n = a.n[mi], S = a.S[mi], L = a.L[mi];
+  const bool tall = a.tall[mi] != 0;
+  const int s_dim = tall ? n : m, l_dim = tall ? m : n;
+  const int q = blockIdx.x * 256 + threadIdx.x;
+  if (q >= s_dim + l_dim) return;
+  double t = 0.0;
+  if (q < s_dim) {
+    const float* rp = a.rpart[mi] + q;  // (L/256) x S, one partial per wide row and column tile
+    for (int k = 0; k < L / kTile; ++k) t += static_cast<double>(rp[static_cast<int64_t>(k) * S]);
+    if (!tall) a.rrms[mi][q] = sqrt(t / n); else a.crms[mi][q] = sqrt(t / m);
+  } else {
+    const int j = q - s_dim;
+    const float* cp = a.cpart[mi] + j;  // (S/256) x L, one partial per wide column and row tile
+    for (int k = 0; k < S / kTile; ++k) t += static_cast<double>(cp[static_cast<int64_t>(k) * L]);
+    if (!tall) a.crms[mi][j] = sqrt(t / m); else a.rrms[mi][j] = sqrt(t / n);
+  }
+}
+
+// One block per matrix: CVs of r and c over entries above delta (eq. "cv", double, two
+// passes), the direction (rows iff gamma_r >= gamma_c, eq. "hidden") and the scale
+// vector of N_r or N_c (eq. "operators"; entries at or below delta get scale 0).
 __global__ __launch_bounds__(256) void k_select(SelectArgs a) {
   __shared__ double red[4];
   const int mi = blockIdx.x;
-  const int m = a.m[mi], n = a.n[mi], S = a.S[mi], L = a.L[mi];
-  const bool tall = a.tall[mi] != 0;
-  const float* rpart = a.rpart[mi];  // (L/256) x S : per wide row
-  const float* cpart = a.cpart[mi];  // (S/256) x L : per wide column
-  const int nct = L / kTile, nrt = S / kTile;
-  double* rr = a.rrms[mi];
-  double* cc = a.crms[mi];
-  // wide row sums
-  const int s_dim = tall ? n : m;
-  const int l_dim = tall ? m : n;
-  for (int i = threadIdx.x; i < s_dim; i += 256) {
-    double t = 0.0;
-    for (int k = 0; k < nct; ++k) t += static_cast<double>(rpart[static_cast<int64_t>(k) * S + i]);
-    // wide row i is own row i (wide) or own column i (tall); divide by the own-orientation length
-    if (!tall) rr[i] = sqrt(t / n); else cc[i] = sqrt(t / m);
-  }
-  for (int j = threadIdx.x; j < l_dim; j += 256) {
-    double t = 0.0;
-    for (int k = 0; k < nrt; ++k) t += static_cast<double>(cpart[static_cast<int64_t>(k) * L + j]);
-    if (!tall) cc[j] = sqrt(t / m); else rr[j] = sqrt(t / n);
-  }
-  __syncthreads();
-  __threadfence_block();
+  const int m = a.m[mi], n = a.n[mi];
+  const double* rr = a.rrms[mi];
+  const double* cc = a.crms[mi];
   const double gr = cv_of(rr, m, a.delta, red);
   const double gc = cv_of(cc, n, a.delta, red);
   const int dir = gr >= gc ? 0 : 1;
@@ -369,6 +373,11 @@ hipError_t launch_norm(const NormArgs& a, hipStream_t st) {
 
 hipError_t launch_rowcol(const RowColArgs& a, int batch, hipStream_t st) {
   hipLaunchKernelGGL(k_rowcol, dim3(a.tiles_r * a.tiles_c, batch), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rms(const SelectArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_rms, dim3((a.max_lines + 255) / 256, a.count), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -363,54 +363,77 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     }
     MEQ_TRY(timed_launch(p, MEQ_K_NORM, st, [&] { return launch_norm(a, st); }));
   }
-  // 3. Newton-Schulz, batched per shape group (ping-pong between buffers a and b).
+  // 3. Newton-Schulz: per step one launch per product over all shape groups (chunks of
+  //    kMaxGemmGroups), longest K first so the long tiles start first.  Ping-pong between
+  //    buffers a (holding X_0) and b.
+  std::vector<int> order(p->groups.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int>(i);
+  for (int k = 0; k < hp.ns_steps; ++k) {
+    const bool from_a = (k % 2) == 0;
+    for (int kind = 0; kind < 3; ++kind) {
+      // kind 0: Gram (K = L), 1: polynomial (K = S), 2: apply (K = S)
+      std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+        const GroupInfo& gx = p->groups[x];
+        const GroupInfo& gy = p->groups[y];
+        const int64_t kx = kind == 0 ? gx.L : gx.S, ky = kind == 0 ? gy.L : gy.S;
+        return kx > ky;
+      });
+      for (size_t c0 = 0; c0 < order.size(); c0 += kMaxGemmGroups) {
+        GemmArgs ga{};
+        ga.count = static_cast<int>(std::min<size_t>(kMaxGemmGroups, order.size() - c0));
+        ga.scale_kind = k == 0 ? (kind == 0 ? 2 : kind == 2 ? 1 : 0) : 0;
+        ga.alpha_e = kind == 0 ? 0.f : kind == 1 ? hp.ns_b : hp.ns_a;
+        ga.alpha_acc = kind == 1 ? hp.ns_c : 1.f;
+        int start = 0;
+        for (int q = 0; q < ga.count; ++q) {
+          const GroupInfo& g = p->groups[order[c0 + q]];
+          const int batch = static_cast<int>(g.mats.size());
+          const int tm = static_cast<int>(g.S / kTile), tn = static_cast<int>(g.L / kTile);
+          uint16_t* cur = reinterpret_cast<uint16_t*>(ws + (from_a ? g.off_xa : g.off_xb));
+          uint16_t* nxt = reinterpret_cast<uint16_t*>(ws + (from_a ? g.off_xb : g.off_xa));
+          uint16_t* am = reinterpret_cast<uint16_t*>(ws + g.off_a);
+          uint16_t* pm = reinterpret_cast<uint16_t*>(ws + g.off_p);
+          GemmGroup& gg = ga.grp[q];
+          gg.fold = reinterpret_cast<const float*>(ws + g.off_fold);
+          if (kind == 0) {  // A = X X^T
+            gg.a = cur; gg.lda = static_cast<int>(g.L); gg.stride_a = g.stride_x;
+            gg.b = cur; gg.ldb = static_cast<int>(g.L); gg.stride_b = g.stride_x;
+            gg.c = am; gg.ldc = static_cast<int>(g.S); gg.stride_c = g.stride_a;
+            gg.e = nullptr; gg.lde = 0; gg.stride_e = 0;
+            gg.K = static_cast<int>(g.L);
+            gg.tiles_m = tm; gg.tiles_n = tm; gg.tiles_per_mat = tm * (tm + 1) / 2;
+          } else if (kind == 1) {  // P = b A + c A A
+            gg.a = am; gg.lda = static_cast<int>(g.S); gg.stride_a = g.stride_a;
+            gg.b = am; gg.ldb = static_cast<int>(g.S); gg.stride_b = g.stride_a;
+            gg.c = pm; gg.ldc = static_cast<int>(g.S); gg.stride_c = g.stride_a;
+            gg.e = am; gg.lde = static_cast<int>(g.S); gg.stride_e = g.stride_a;
+            gg.K = static_cast<int>(g.S);
+            gg.tiles_m = tm; gg.tiles_n = tm; gg.tiles_per_mat = tm * (tm + 1) / 2;
+          } else {  // X <- a X + P X
+            gg.a = pm; gg.lda = static_cast<int>(g.S); gg.stride_a = g.stride_a;
+            gg.b = cur; gg.ldb = static_cast<int>(g.L); gg.stride_b = g.stride_x;
+            gg.c = nxt; gg.ldc = static_cast<int>(g.L); gg.stride_c = g.stride_x;
+            gg.e = cur; gg.lde = static_cast<int>(g.L); gg.stride_e = g.stride_x;
+            gg.K = static_cast<int>(g.S);
+            gg.tiles_m = tm; gg.tiles_n = tn; gg.tiles_per_mat = tm * tn;
+          }
+          gg.tiles = gg.tiles_per_mat * batch;
+          ga.tile_start[q] = start;
+          start += (gg.tiles + 7) / 8 * 8;
+        }
+        ga.tile_start[ga.count] = start;
+        const int kk = kind == 0 ? MEQ_K_GRAM : kind == 1 ? MEQ_K_POLY : MEQ_K_APPLY;
+        MEQ_TRY(timed_launch(p, kk, st, [&] { return launch_gemm(ga, kind, st); }));
+      }
+    }
+  }
+  // 4. row / column sums of squares of U, per shape group
   for (size_t gi = 0; gi < p->groups.size(); ++gi) {
     const GroupInfo& g = p->groups[gi];
     const int batch = static_cast<int>(g.mats.size());
     const int tm = static_cast<int>(g.S / kTile), tn = static_cast<int>(g.L / kTile);
     uint16_t* xa = reinterpret_cast<uint16_t*>(ws + g.off_xa);
     uint16_t* xb = reinterpret_cast<uint16_t*>(ws + g.off_xb);
-    uint16_t* am = reinterpret_cast<uint16_t*>(ws + g.off_a);
-    uint16_t* pm = reinterpret_cast<uint16_t*>(ws + g.off_p);
-    const float* fold = reinterpret_cast<const float*>(ws + g.off_fold);
-    uint16_t* cur = xa;
-    uint16_t* nxt = xb;
-    for (int k = 0; k < hp.ns_steps; ++k) {
-      GemmArgs ga{};
-      ga.a = cur; ga.lda = g.L; ga.stride_a = g.stride_x;
-      ga.b = cur; ga.ldb = g.L; ga.stride_b = g.stride_x;
-      ga.c = am; ga.ldc = g.S; ga.stride_c = g.stride_a;
-      ga.e = nullptr;
-      ga.fold = fold; ga.scale_kind = k == 0 ? 2 : 0;
-      ga.alpha_e = 0.f; ga.alpha_acc = 1.f;
-      ga.M = static_cast<int>(g.S); ga.N = static_cast<int>(g.S); ga.K = static_cast<int>(g.L);
-      ga.tiles_m = tm; ga.tiles_n = tm; ga.tiles_per_mat = tm * (tm + 1) / 2; ga.batch = batch;
-      MEQ_TRY(timed_launch(p, MEQ_K_GRAM, st, [&] { return launch_gemm(ga, 0, st); }));
-
-      GemmArgs gp{};
-      gp.a = am; gp.lda = g.S; gp.stride_a = g.stride_a;
-      gp.b = am; gp.ldb = g.S; gp.stride_b = g.stride_a;
-      gp.c = pm; gp.ldc = g.S; gp.stride_c = g.stride_a;
-      gp.e = am; gp.lde = g.S; gp.stride_e = g.stride_a;
-      gp.fold = fold; gp.scale_kind = 0;
-      gp.alpha_e = hp.ns_b; gp.alpha_acc = hp.ns_c;
-      gp.M = static_cast<int>(g.S); gp.N = static_cast<int>(g.S); gp.K = static_cast<int>(g.S);
-      gp.tiles_m = tm; gp.tiles_n = tm; gp.tiles_per_mat = tm * (tm + 1) / 2; gp.batch = batch;
-      MEQ_TRY(timed_launch(p, MEQ_K_POLY, st, [&] { return launch_gemm(gp, 1, st); }));
-
-      GemmArgs gx{};
-      gx.a = pm; gx.lda = g.S; gx.stride_a = g.stride_a;
-      gx.b = cur; gx.ldb = g.L; gx.stride_b = g.stride_x;
-      gx.c = nxt; gx.ldc = g.L; gx.stride_c = g.stride_x;
-      gx.e = cur; gx.lde = g.L; gx.stride_e = g.stride_x;
-      gx.fold = fold; gx.scale_kind = k == 0 ? 1 : 0;
-      gx.alpha_e = hp.ns_a; gx.alpha_acc = 1.f;
-      gx.M = static_cast<int>(g.S); gx.N = static_cast<int>(g.L); gx.K = static_cast<int>(g.S);
-      gx.tiles_m = tm; gx.tiles_n = tn; gx.tiles_per_mat = tm * tn; gx.batch = batch;
-      MEQ_TRY(timed_launch(p, MEQ_K_APPLY, st, [&] { return launch_gemm(gx, 2, st); }));
-      std::swap(cur, nxt);
-    }
-    // 4. row / column sums of squares of U
     RowColArgs rc{};
     rc.u = (hp.ns_steps % 2 == 1) ? xb : xa;
     rc.stride_u = g.stride_x;
@@ -424,7 +447,7 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     rc.tiles_c = tn;
     MEQ_TRY(timed_launch(p, MEQ_K_ROWCOL, st, [&] { return launch_rowcol(rc, batch, st); }));
   }
-  // 5. CVs, direction, scale vectors
+  // 5. row/column RMS, CVs, direction, scale vectors
   for (int c0 = 0; c0 < count; c0 += kMaxChunk) {
     SelectArgs a{};
     a.count = std::min(kMaxChunk, count - c0);
@@ -443,7 +466,9 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
       a.crms[k] = reinterpret_cast<double*>(ws + mi.off_crms);
       a.scale[k] = reinterpret_cast<float*>(ws + mi.off_scale);
       a.scal[k] = scal + c0 + k;
+      a.max_lines = std::max(a.max_lines, static_cast<int>(mi.s + mi.l));
     }
+    MEQ_TRY(timed_launch(p, MEQ_K_SELECT, st, [&] { return launch_rms(a, st); }));
     MEQ_TRY(timed_launch(p, MEQ_K_SELECT, st, [&] { return launch_select(a, st); }));
   }
   // 6. write-back

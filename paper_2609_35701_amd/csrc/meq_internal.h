@@ -53,25 +53,32 @@ struct NormArgs {
 };
 
 // ------------------------------------------------------------------------ NS GEMMs
-// C = s * (alpha_e * E + alpha_acc * (Aop . Bop)) stored as bf16, batched over
-// the matrices of one shape group.  Aop is M x K row-major.  Bop is N x K
-// row-major (NT) or K x N row-major (NN).  For the symmetric products only tiles
-// on or above the diagonal are computed and each off-diagonal tile is also
-// stored mirrored.
-struct GemmArgs {
+// C = s * (alpha_e * E + alpha_acc * (Aop . Bop)) stored as bf16, batched over the
+// matrices of a shape group; one launch covers up to kMaxGemmGroups groups.  Aop is
+// M x K row-major.  Bop is N x K row-major (NT) or K x N row-major (NN).  For the
+// symmetric products only tiles on or above the diagonal are computed and each
+// off-diagonal tile is also stored mirrored.
+constexpr int kMaxGemmGroups = 8;
+
+struct GemmGroup {
   const uint16_t* a;
-  int64_t lda, stride_a;
   const uint16_t* b;
-  int64_t ldb, stride_b;
   uint16_t* c;
-  int64_t ldc, stride_c;
-  const uint16_t* e;  // may be null when alpha_e == 0
-  int64_t lde, stride_e;
-  const float* fold;  // per batch member: (1/||V||, 1/||V||^2)
-  int scale_kind;     // 0 none, 1 scale by 1/||V||, 2 scale by 1/||V||^2
+  const uint16_t* e;   // null when alpha_e == 0
+  const float* fold;   // per batch member: (1/||V||, 1/||V||^2)
+  int64_t stride_a, stride_b, stride_c, stride_e;  // elements per matrix
+  int lda, ldb, ldc, lde;
+  int K;
+  int tiles_m, tiles_n, tiles_per_mat;
+  int tiles;           // batch * tiles_per_mat
+};
+
+struct GemmArgs {
+  int count;                             // groups in this launch
+  int scale_kind;                        // 0 none, 1 scale by 1/||V||, 2 scale by 1/||V||^2
   float alpha_e, alpha_acc;
-  int M, N, K;
-  int tiles_m, tiles_n, tiles_per_mat, batch;
+  int tile_start[kMaxGemmGroups + 1];    // workgroup ranges per group, multiples of 8
+  GemmGroup grp[kMaxGemmGroups];
 };
 
 // ----------------------------------------------------------------- row/col sums of U
@@ -87,9 +94,11 @@ struct RowColArgs {
 };
 
 // ------------------------------------------------------------------ CV + direction
+// Also used by the row/column RMS finalization (one launch per chunk of matrices).
 struct SelectArgs {
   int count;
   double delta;
+  int max_lines;  // max over the chunk of s + l (wide rows + wide columns)
   int m[kMaxChunk], n[kMaxChunk], tall[kMaxChunk], S[kMaxChunk], L[kMaxChunk];
   const float* rpart[kMaxChunk];
   const float* cpart[kMaxChunk];
@@ -118,6 +127,7 @@ hipError_t launch_momentum(const MomentumArgs& a, int grad_bf16, int total_tiles
 hipError_t launch_norm(const NormArgs& a, hipStream_t st);
 hipError_t launch_gemm(const GemmArgs& a, int mode, hipStream_t st);  // 0 Gram, 1 poly, 2 apply
 hipError_t launch_rowcol(const RowColArgs& a, int batch, hipStream_t st);
+hipError_t launch_rms(const SelectArgs& a, hipStream_t st);
 hipError_t launch_select(const SelectArgs& a, hipStream_t st);
 hipError_t launch_update(const UpdateArgs& a, int param_bf16, int total_tiles, hipStream_t st);
 
