@@ -1,7 +1,9 @@
 // Newton-Schulz products on bf16 MFMA (gfx950), eq. "ns":
 //   A_k = X_k X_k^T                (NT, symmetric: tiles on or above the diagonal + mirrored store)
-//   P_k = b A_k + c A_k A_k        (NT since A_k is symmetric; symmetric output)
-//   X_{k+1} = a X_k + P_k X_k      (NN: X_k is staged K-major and read with LDS transpose reads)
+//   P_k = a I + b A_k + c A_k A_k  (NT since A_k is symmetric; symmetric output)
+//   X_{k+1} = P_k X_k              (NN: X_k is staged K-major and read with LDS transpose reads)
+// which is a X_k + (b A_k + c A_k A_k) X_k regrouped: the a X_k term rides on the
+// diagonal of P_k, so the apply epilogue reads nothing besides its accumulators.
 // X_0 = V / ||V||_F is folded in: the bf16 buffer holds V, the k = 0 Gram epilogue
 // scales by 1/||V||^2 and the k = 0 apply epilogue by 1/||V||.
 //
@@ -11,7 +13,7 @@
 // one is consumed, which covers the latency of the loads that miss L2).  Global ->
 // LDS traffic uses buffer loads that write LDS directly (no registers, no LDS store
 // instructions); 16-byte chunks are XOR-swizzled so fragment reads are free of bank
-// conflicts.  The epilogue stages the output tile (and the tile it adds, X or A) in
+// conflicts.  The epilogue stages the output tile (and, for P, the A tile it adds) in
 // LDS and writes whole rows with 16-byte stores.  Same-shape matrices form one
 // launch; workgroup ids are remapped so each XCD receives a contiguous run of tiles.
 #include "meq_internal.h"
@@ -104,7 +106,7 @@ template <int kMode>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_ns_gemm(GemmArgs args) {
   constexpr bool kNN = kMode == 2;
   constexpr bool kSym = kMode != 2;
-  constexpr bool kHasE = kMode != 0;
+  constexpr bool kHasE = kMode == 1;
   // Four ring stages as separate objects, so the compiler can tell the stage being read
   // from the stages being filled.
   __shared__ __attribute__((aligned(1024))) uint8_t st0_[kStageBytes];
@@ -305,6 +307,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   float s = 1.f;
   if (args.scale_kind != 0) s = g.fold[2 * mat + (args.scale_kind - 1)];
   const float ae = args.alpha_e * s, aa = args.alpha_acc * s;
+  const float ad = (kSym && ti == tj) ? args.alpha_diag * s : 0.f;  // diagonal tiles only
   const int own_row = kNN ? wm : wn;  // 128-row half holding this wave's OUT rows
   const int own_col = kNN ? wn : wm;  // 128-column half holding this wave's OUT columns
   const int ldo = g.ldc;
@@ -350,6 +353,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           o[1] = fmaf(ae, bf16_to_f32(e.x >> 16), o[1]);
           o[2] = fmaf(ae, bf16_to_f32(e.y & 0xffffu), o[2]);
           o[3] = fmaf(ae, bf16_to_f32(e.y >> 16), o[3]);
+        }
+        if (kSym) {
+          // OUT is symmetric here, so OUT[r][c + q] is on the diagonal when r == c + q
+#pragma unroll
+          for (int q = 0; q < 4; ++q) o[q] += (r == c + q) ? ad : 0.f;
         }
         packed[i][j][vq].x = pack_bf16x2(o[0], o[1]);
         packed[i][j][vq].y = pack_bf16x2(o[2], o[3]);

@@ -382,8 +382,11 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
         GemmArgs ga{};
         ga.count = static_cast<int>(std::min<size_t>(kMaxGemmGroups, order.size() - c0));
         ga.scale_kind = k == 0 ? (kind == 0 ? 2 : kind == 2 ? 1 : 0) : 0;
-        ga.alpha_e = kind == 0 ? 0.f : kind == 1 ? hp.ns_b : hp.ns_a;
+        // The a X term of X <- a X + P X is carried by P: the polynomial product stores
+        // a I + b A + c A A, and the apply product is the plain product (a I + P) X.
+        ga.alpha_e = kind == 1 ? hp.ns_b : 0.f;
         ga.alpha_acc = kind == 1 ? hp.ns_c : 1.f;
+        ga.alpha_diag = kind == 1 ? hp.ns_a : 0.f;
         int start = 0;
         for (int q = 0; q < ga.count; ++q) {
           const GroupInfo& g = p->groups[order[c0 + q]];
@@ -402,18 +405,18 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
             gg.e = nullptr; gg.lde = 0; gg.stride_e = 0;
             gg.K = static_cast<int>(g.L);
             gg.tiles_m = tm; gg.tiles_n = tm; gg.tiles_per_mat = tm * (tm + 1) / 2;
-          } else if (kind == 1) {  // P = b A + c A A
+          } else if (kind == 1) {  // P = a I + b A + c A A
             gg.a = am; gg.lda = static_cast<int>(g.S); gg.stride_a = g.stride_a;
             gg.b = am; gg.ldb = static_cast<int>(g.S); gg.stride_b = g.stride_a;
             gg.c = pm; gg.ldc = static_cast<int>(g.S); gg.stride_c = g.stride_a;
             gg.e = am; gg.lde = static_cast<int>(g.S); gg.stride_e = g.stride_a;
             gg.K = static_cast<int>(g.S);
             gg.tiles_m = tm; gg.tiles_n = tm; gg.tiles_per_mat = tm * (tm + 1) / 2;
-          } else {  // X <- a X + P X
+          } else {  // X <- (a I + b A + c A A) X
             gg.a = pm; gg.lda = static_cast<int>(g.S); gg.stride_a = g.stride_a;
             gg.b = cur; gg.ldb = static_cast<int>(g.L); gg.stride_b = g.stride_x;
             gg.c = nxt; gg.ldc = static_cast<int>(g.L); gg.stride_c = g.stride_x;
-            gg.e = cur; gg.lde = static_cast<int>(g.L); gg.stride_e = g.stride_x;
+            gg.e = nullptr; gg.lde = 0; gg.stride_e = 0;
             gg.K = static_cast<int>(g.S);
             gg.tiles_m = tm; gg.tiles_n = tn; gg.tiles_per_mat = tm * tn;
           }

@@ -53,7 +53,7 @@ struct NormArgs {
 };
 
 // ------------------------------------------------------------------------ NS GEMMs
-// C = s * (alpha_e * E + alpha_acc * (Aop . Bop)) stored as bf16, batched over the
+// C = s * (alpha_e * E + alpha_acc * (Aop . Bop) + alpha_diag * I) stored as bf16, batched over the
 // matrices of a shape group; one launch covers up to kMaxGemmGroups groups.  Aop is
 // M x K row-major.  Bop is N x K row-major (NT) or K x N row-major (NN).  For the
 // symmetric products only tiles on or above the diagonal are computed and each
@@ -77,6 +77,7 @@ struct GemmArgs {
   int count;                             // groups in this launch
   int scale_kind;                        // 0 none, 1 scale by 1/||V||, 2 scale by 1/||V||^2
   float alpha_e, alpha_acc;
+  float alpha_diag;                      // symmetric products only
   int tile_start[kMaxGemmGroups + 1];    // workgroup ranges per group, multiples of 8
   GemmGroup grp[kMaxGemmGroups];
 };
