@@ -208,11 +208,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int nn_k = 8 * (grp >> 1) + (jq >> 2);                // + 16 kk + 4 t
   const int nn_n = wn * 128 + 16 * (grp & 1) + 4 * (jq & 3);  // + 32 j
   const int nn_swz = 4 * (nn_k & 3);
-  auto nn_addr = [&](int kk, int t4, int j) {
-    const int k = 16 * kk + nn_k + 4 * t4;
+  // Lane part of the address of column block j.  Rows k + 16 kk + 4 t lie (16 kk + 4 t) * 512
+  // bytes further with the same swizzle (it depends on k & 3 only).  One precomputed offset
+  // per block keeps every read a short constant step from its stage array, which is what
+  // lets the compiler tell the stages apart when it places waits for the LDS-bound loads.
+  int nn_off[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
     const int n = nn_n + 32 * j;
-    return 16384 + k * 512 + 16 * ((n >> 3) ^ nn_swz) + 2 * (n & 7);
-  };
+    nn_off[j] = nn_k * 512 + 16 * ((n >> 3) ^ nn_swz) + 2 * (n & 7);
+  }
 
   floatx16 acc[4][4];
 #pragma unroll
@@ -223,19 +228,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   auto load_frags = [&](const lds_u8* buf, int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[4]) {
+    const int oa = offA + slot_kk[kk];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(buf + offA + i * 2048 + slot_kk[kk]);
+    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(buf + oa + i * 2048);
     if (kNN) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + nn_addr(kk, 0, j)));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + nn_addr(kk, 1, j)));
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + (nn_off[j] + 16384 + 8192 * kk)));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + (nn_off[j] + 18432 + 8192 * kk)));
         bfr[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
     } else {
+      const int ob = offB_nt + slot_kk[kk];
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        bfr[j] = *reinterpret_cast<const lds_bf16x8*>(buf + offB_nt + j * 2048 + slot_kk[kk]);
+      for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const lds_bf16x8*>(buf + ob + j * 2048);
     }
   };
 
