@@ -8,8 +8,11 @@ and gradients, fp32 momentum, inputs resident in HBM.  Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -20,6 +23,119 @@ if ROOT not in sys.path:
 METRIC = "MeqMuon steps/sec over all hidden 2D weights (1B shape); NS MFMA %, norm GB/s"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+GEMM_SOURCE = os.path.join(ROOT, "paper_2609_35701_amd", "csrc", "k_ns_gemm.hip")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "k_ns_gemm_apply_llama1b_traffic.md")
+CALIBRATION_BYTES = 256 << 20  # the plain copy kernel of known size: 256 MiB read + 256 MiB written
+CALIBRATION_KERNEL = "neg_kernel"  # torch.neg on fp32 is the copy (one read, one write per element)
+
+
+def gemm_source_hash() -> str:
+    with open(GEMM_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per apply launch from the committed counter summary, or None when that summary
+    is missing, was taken on another workload or on another version of the GEMM source."""
+    if workload != "llama-1b" or not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    fields = {}
+    with open(TRAFFIC_PROFILE) as f:
+        for line in f:
+            m = re.match(r"^- (\w+): (\S+)\s*$", line)
+            if m:
+                fields[m.group(1)] = m.group(2)
+    if fields.get("kernel_source_sha256") != gemm_source_hash():
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def _kernel_key(name: str) -> str:
+    if CALIBRATION_KERNEL in name:
+        return CALIBRATION_KERNEL
+    m = re.search(r"meq::(?:\(anonymous namespace\)::)?(k_\w+(<[^>]*>)?)\(", name)
+    if m:
+        return m.group(1)
+    return "torch: " + name.split("<")[0][:50]
+
+
+def _counter_means(run_dir: str, counter: str):
+    """Mean value of one rocprofv3 --pmc counter per dispatch, by kernel."""
+    path = os.path.join(run_dir, "run_counter_collection.csv")
+    tot, disp = {}, {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            k = _kernel_key(r["Kernel_Name"])
+            tot[k] = tot.get(k, 0.0) + float(r["Counter_Value"])
+            disp.setdefault(k, set()).add(r["Dispatch_Id"])
+    return {k: (tot[k] / len(disp[k]), len(disp[k])) for k in tot}
+
+
+def summarize_traffic(fetch_dir: str, write_dir: str, out: str, fetch_cmd: str, write_cmd: str) -> None:
+    """Write the apply kernel's HBM traffic summary from two counter runs (FETCH_SIZE, WRITE_SIZE).
+
+    Both counters are in KiB per dispatch.  Each is divided by what it reads, per byte, for the
+    calibration copy of known size, so the result is in bytes the copy would have moved."""
+    fe = _counter_means(fetch_dir, "FETCH_SIZE")
+    wr = _counter_means(write_dir, "WRITE_SIZE")
+    cf = fe[CALIBRATION_KERNEL][0] * 1024 / CALIBRATION_BYTES
+    cw = wr[CALIBRATION_KERNEL][0] * 1024 / CALIBRATION_BYTES
+    rows = []
+    for k in sorted(set(fe) | set(wr)):
+        f_kib, n = fe.get(k, (float("nan"), 0))
+        w_kib, _ = wr.get(k, (float("nan"), 0))
+        rows.append((k, n, f_kib, w_kib, f_kib * 1024 / cf + w_kib * 1024 / cw))
+    apply = [r for r in rows if r[0] == "k_ns_gemm<2>"][0]
+    lines = [
+        "# HBM traffic per dispatch (rocprofv3 FETCH_SIZE / WRITE_SIZE), llama-1b step\n\n",
+        "Commands (from the repository root on one MI355X; each counter in a run of its own):\n\n",
+        f"    {fetch_cmd}\n    {write_cmd}\n\n",
+        "Summarised with `python bench.py --summarize-traffic <fetch dir> <write dir> --out <this file>`.\n",
+        f"Calibration: torch.neg over {CALIBRATION_BYTES >> 20} MiB of fp32 (one read and one write of "
+        f"{CALIBRATION_BYTES >> 20} MiB) reads FETCH_SIZE {fe[CALIBRATION_KERNEL][0]:.0f} KiB and WRITE_SIZE "
+        f"{wr[CALIBRATION_KERNEL][0]:.0f} KiB, i.e. factors {cf:.4f} (fetch) and {cw:.4f} (write) per byte moved; "
+        "kernel figures below are divided by these factors.\n\n",
+        "| kernel | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch | calibrated bytes/dispatch |\n",
+        "|---|---|---|---|---|\n",
+    ]
+    for k, n, f_kib, w_kib, b in rows:
+        lines.append(f"| {k} | {n} | {f_kib:.0f} | {w_kib:.0f} | {b:.4g} |\n")
+    lines += [
+        "\nRecorded for the benchmark's roofline (apply product, k_ns_gemm<2>):\n\n",
+        f"- traffic_bytes_per_launch: {apply[4]:.6g}\n",
+        f"- kernel_source_sha256: {gemm_source_hash()}\n",
+    ]
+    with open(out, "w") as f:
+        f.write("".join(lines))
+
+
+def summarize_stats(stats_csv: str, out: str, command: str, note: str) -> None:
+    """Markdown table of a rocprofv3 --kernel-trace --stats run."""
+    with open(stats_csv) as f:
+        rows = list(csv.DictReader(f))
+
+    def short(n):
+        n = re.sub(r"\(anonymous namespace\)::", "", n)
+        if "at::native" in n:
+            return "torch: " + n.split("<")[0][:60]
+        return n[:90]
+
+    lines = ["# rocprofv3 kernel stats\n\n", "Command (from the repository root on one MI355X):\n\n",
+             f"    {command}\n\n"]
+    if note:
+        lines.append(note + "\n\n")
+    lines.append("| kernel | calls | total ms | avg ms | min ms | max ms | % |\n|---|---|---|---|---|---|---|\n")
+    for r in rows:
+        lines.append(f"| {short(r['Name'])} | {r['Calls']} | {int(r['TotalDurationNs']) / 1e6:.3f} | "
+                     f"{float(r['AverageNs']) / 1e6:.4f} | {int(r['MinNs']) / 1e6:.4f} | "
+                     f"{int(r['MaxNs']) / 1e6:.4f} | {float(r['Percentage']):.2f} |\n")
+    with open(out, "w") as f:
+        f.write("".join(lines))
 
 
 def ns_flops(s: int, l: int, steps: int):
@@ -86,9 +202,24 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=30.0, help="seconds of oracle work at most")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="run one plain 256 MiB device-to-device copy before the warm-up, as the reference "
-                         "kernel of known size for FETCH_SIZE / WRITE_SIZE counter runs")
+                    help="run one plain copy kernel of known size (torch.neg over 256 MiB of fp32) before the "
+                         "warm-up, as the reference for FETCH_SIZE / WRITE_SIZE counter runs")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) into --out and exit")
+    ap.add_argument("--summarize-stats", metavar="STATS_CSV",
+                    help="summarise a rocprofv3 --kernel-trace --stats run into --out and exit")
+    ap.add_argument("--out")
+    ap.add_argument("--command", default="", help="command line(s) recorded in a summary ('|' separates two)")
+    ap.add_argument("--note", default="")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        cmds = args.command.split("|") + ["", ""]
+        summarize_traffic(args.summarize_traffic[0], args.summarize_traffic[1], args.out, cmds[0].strip(),
+                          cmds[1].strip())
+        return 0
+    if args.summarize_stats:
+        summarize_stats(args.summarize_stats, args.out, args.command, args.note)
+        return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the MeqMuon update is measured on a single MI355X; "
               f"--gpus {args.gpus} is not supported (multi-GPU sharding is a design note, not built)",
@@ -112,9 +243,9 @@ def main() -> int:
     print(f"# bench: workspace {upd.plan.workspace_bytes / 2**30:.2f} GiB, groups {upd.plan.groups()}",
           file=sys.stderr, flush=True)
     if args.copy_calibration:
-        src = torch.ones(256 << 20, dtype=torch.uint8, device=dev)
+        src = torch.ones(CALIBRATION_BYTES // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
     for _ in range(args.warmup):
@@ -152,7 +283,7 @@ def main() -> int:
     apply_tflops = apply / (ap_ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "kernel": "k_ns_gemm<2> (X <- aX + P X, bf16 MFMA)",
                 "achieved": apply_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": apply_tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                "frac": apply_tflops / PEAK_BF16_TFLOPS, "traffic": recorded_traffic(wl.name),
                 "flops_per_launch": apply / max(kern["apply"]["launches_per_step"], 1),
                 "avg_launch_ms": kern["apply"]["avg_launch_ms"]}
     stages = {
