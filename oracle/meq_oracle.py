@@ -1,4 +1,5 @@
-"""fp64 CPU oracle of the MeqMuon update for 2D hidden-layer weights.
+"""fp64 CPU oracle of the MeqMuon update (hidden 2D weights, remaining 2D parameters,
+1-D parameters) and of the Moonlight-Muon update it is compared with.
 
 TEST INFRASTRUCTURE ONLY.  This module is the plain, slow definition that the
 HIP path is checked against.  Only the tests, the package's ``smoke()`` check
@@ -18,7 +19,13 @@ Readings where the paper is silent (all listed, with reasons, in the design note
 * RMS values at or below delta count as zero both in the CVs (eq. "cv") and in
   the row/column operators (eq. "operators"), i.e. such a row gets scale 0;
 * a CV over no nonzero entry is 0;
-* the direction tie gamma_r == gamma_c selects rows (eq. "hidden" uses >=).
+* the direction tie gamma_r == gamma_c selects rows (eq. "hidden" uses >=);
+* remaining 2D parameters and 1-D parameters use the same momentum as the hidden
+  weights (Algorithm "MeqMuon" has one momentum rule); ``nesterov`` applies to them
+  only if set, since the paper states Nesterov momentum for the hidden weights only;
+* decoupled weight decay applies to every parameter kind, as the algorithm's last
+  line does;
+* a zero 1-D momentum gives a zero update (the global RMS is then 0).
 
 Parity pins: every function here is pinned by tests in ``tests/test_oracle_pins.py``
 against closed forms, SVD, invariances and brute force; none is "parity unpinned".
@@ -208,3 +215,64 @@ def meq_step(w: np.ndarray, g: np.ndarray, b_prev: np.ndarray, hp: HParams, lr: 
     w_new = write_back(w, ut, lr, hp.rho, hp.weight_decay)
     return {"W": w_new, "B": b, "V": v, "normsq": frobenius(v) ** 2, "U": u, "Ut": ut,
             "gamma_r": gr, "gamma_c": gc, "dir": d}
+
+
+# ------------------------------------------------- remaining 2D parameters (eq. "aux")
+def two_sided(v: np.ndarray, delta: float):
+    """U~ = N_c(N_r(V))  (eq. "aux").
+
+    Rows of V are scaled to unit RMS first; the column RMS is then taken of that
+    row-normalized matrix.  Rows or columns with RMS <= delta stay zero.
+    Returns (U~, r of V, c of N_r(V)).
+    """
+    v = np.asarray(v, np.float64)
+    r, _ = row_col_rms(v)
+    vr = row_normalize(v, delta)
+    _, c = row_col_rms(vr)
+    return col_normalize(vr, delta), r, c
+
+
+def aux_step(w: np.ndarray, g: np.ndarray, b_prev: np.ndarray, hp: HParams, lr: float) -> dict:
+    """One MeqMuon step for a remaining 2D parameter such as a token embedding or an LM
+    head (Algorithm "MeqMuon", second branch): momentum -> two-sided normalization of the
+    momentum itself (no orthogonalization) -> decoupled-weight-decay write-back."""
+    b = momentum(b_prev, g, hp.mu)
+    v = ns_input(b, g, hp.mu, hp.nesterov)
+    ut, r, c = two_sided(v, hp.delta)
+    w_new = write_back(w, ut, lr, hp.rho, hp.weight_decay)
+    return {"W": w_new, "B": b, "V": v, "r": r, "c": c, "Ut": ut}
+
+
+# ------------------------------------------------------------ 1-D parameters (eq. "vector")
+def global_rms_normalize(v: np.ndarray) -> np.ndarray:
+    """U~ = V / (||V||_2 / sqrt(d))  (eq. "vector"); a zero V gives a zero update."""
+    v = np.asarray(v, np.float64).ravel()
+    nrm = math.sqrt(float(np.sum(v * v)))
+    if nrm == 0.0:
+        return np.zeros_like(v)
+    return v / (nrm / math.sqrt(v.size))
+
+
+def vec_step(w: np.ndarray, g: np.ndarray, b_prev: np.ndarray, hp: HParams, lr: float) -> dict:
+    """One MeqMuon step for a 1-D parameter such as an RMSNorm weight or a bias
+    (Algorithm "MeqMuon", last branch)."""
+    b = momentum(np.ravel(b_prev), np.ravel(g), hp.mu)
+    v = ns_input(b, np.ravel(g), hp.mu, hp.nesterov)
+    ut = global_rms_normalize(v)
+    w_new = write_back(np.ravel(w), ut, lr, hp.rho, hp.weight_decay)
+    return {"W": w_new, "B": b, "V": v, "normsq": float(np.sum(v * v)), "Ut": ut}
+
+
+# ------------------------------------------------------- Moonlight-Muon (eq. "moonlight-update")
+def moonlight_step(w: np.ndarray, g: np.ndarray, b_prev: np.ndarray, hp: HParams, lr: float,
+                   wide: bool = False) -> dict:
+    """One Muon step in the Moonlight form the paper compares with (eq. "moonlight-update"):
+    U = Orth(B) by the same K Newton-Schulz steps, then
+    W_{t+1} = (1 - eta lambda) W - eta rho sqrt(max(m, n)) U, with no equilibration."""
+    b = momentum(b_prev, g, hp.mu)
+    v = ns_input(b, g, hp.mu, hp.nesterov)
+    u = newton_schulz(v, hp.ns_a, hp.ns_b, hp.ns_c, hp.ns_steps, wide=wide)
+    m, n = u.shape
+    ut = math.sqrt(max(m, n)) * u
+    w_new = write_back(w, ut, lr, hp.rho, hp.weight_decay)
+    return {"W": w_new, "B": b, "V": v, "normsq": frobenius(v) ** 2, "U": u, "Ut": ut}
