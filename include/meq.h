@@ -1,16 +1,25 @@
 /*
- * meq.h - C ABI of the MeqMuon hidden-weight update for AMD MI355X (gfx950).
+ * meq.h - C ABI of the MeqMuon optimizer update for AMD MI355X (gfx950).
  *
- * One call of meq_step performs, for every 2D hidden-layer weight W (m x n,
- * row-major, rows = output features), the hidden-weight branch of the paper's
- * Algorithm "MeqMuon" (arxiv 2609.35701, Section "MeqMuon"):
+ * One call of meq_step updates every parameter of a plan.  A plan holds one kind
+ * of parameter (Algorithm "MeqMuon", arxiv 2609.35701, Section "MeqMuon"); all
+ * kinds share the momentum and the write-back:
  *
  *   B   <- mu * B + G                                   eq. "momentum"
  *   V   <- B            (or G + mu * B when nesterov)   Section "Experiments"
- *   U   <- K quintic Newton-Schulz steps on V / ||V||_F eq. "ns"
- *   r,c <- row / column RMS of U                        eq. "row-col-rms"
- *   U~  <- N_r(U) if CV(r) >= CV(c) else N_c(U)         eqs. "cv", "operators", "hidden"
  *   W   <- (1 - lr * lambda) * W - rho * lr * U~        eq. "meqmuon-update"
+ *
+ * and differ in U~:
+ *   MEQ_PARAM_HIDDEN  2D hidden-layer weight W (m x n, rows = output features):
+ *                       U   <- K quintic Newton-Schulz steps on V / ||V||_F   eq. "ns"
+ *                       r,c <- row / column RMS of U                          eq. "row-col-rms"
+ *                       U~  <- N_r(U) if CV(r) >= CV(c) else N_c(U)           eqs. "cv", "operators", "hidden"
+ *                     or, with update_rule MEQ_RULE_MOONLIGHT, the Muon update the paper
+ *                     compares with: U~ <- sqrt(max(m, n)) * U               eq. "moonlight-update"
+ *   MEQ_PARAM_AUX     remaining 2D parameter (token embedding, LM head; rows = vocabulary):
+ *                       U~  <- N_c(N_r(V))                                    eq. "aux"
+ *   MEQ_PARAM_VECTOR  1-D parameter (norm weight, bias) of d elements:
+ *                       U~  <- V / (||V||_2 / sqrt(d))                        eq. "vector"
  *
  * Conventions shared by every entry point
  *   - Matrices are dense, contiguous, row-major; element (i, j) of an m x n
@@ -51,6 +60,14 @@ typedef enum { MEQ_F32 = 0, MEQ_BF16 = 1 } meq_dtype;
 /* Normalization direction chosen for a matrix (eq. "hidden"). */
 typedef enum { MEQ_DIR_ROW = 0, MEQ_DIR_COL = 1 } meq_direction;
 
+/* Parameter kind of a plan (the three branches of Algorithm "MeqMuon"). */
+typedef enum { MEQ_PARAM_HIDDEN = 0, MEQ_PARAM_AUX = 1, MEQ_PARAM_VECTOR = 2 } meq_param_kind;
+
+/* Update of hidden weights: MeqMuon's equilibrated update (eq. "hidden"), or the
+ * Moonlight-Muon update with the sqrt(max(m, n)) factor and no equilibration
+ * (eq. "moonlight-update"), run on the same Newton-Schulz kernels. */
+typedef enum { MEQ_RULE_MEQMUON = 0, MEQ_RULE_MOONLIGHT = 1 } meq_update_rule;
+
 /*
  * Hyperparameters of the update (Section "Experiments"; delta from Section
  * "Imbalance patterns").  The learning rate eta_t is passed to each meq_step.
@@ -60,8 +77,10 @@ typedef enum { MEQ_DIR_ROW = 0, MEQ_DIR_COL = 1 } meq_direction;
  *   ns_steps       number K of Newton-Schulz steps, 1 <= K <= 64
  *   ns_a/b/c       quintic coefficients (a, b, c), finite
  *   zero_rms_delta RMS values at or below delta count as zero, delta >= 0
- *   nesterov       0: orthogonalize B_t (Algorithm "MeqMuon");
- *                  1: orthogonalize G_t + mu * B_t
+ *   nesterov       0: normalize B_t (Algorithm "MeqMuon");
+ *                  1: normalize G_t + mu * B_t (the experiments' hidden weights)
+ *   update_rule    meq_update_rule; MEQ_RULE_MOONLIGHT only for MEQ_PARAM_HIDDEN plans
+ * ns_steps, ns_a/b/c only matter for hidden plans but are validated for every plan.
  */
 typedef struct {
   float mu;
@@ -73,14 +92,18 @@ typedef struct {
   float ns_c;
   float zero_rms_delta;
   int32_t nesterov;
+  int32_t update_rule;
 } meq_hparams;
 
 /*
- * One hidden-layer weight: rows x cols, with its parameter and gradient dtype.
+ * One parameter: rows x cols, with its parameter and gradient dtype.
  * Supported (param, grad) pairs: (MEQ_F32, MEQ_F32) and (MEQ_BF16, MEQ_BF16).
  * The momentum is always float32 with the same shape (one value per element,
  * the paper's optimizer-state accounting in Table "experiment-efficiency").
- * 1 <= rows, cols <= 65536.
+ * Limits by plan kind:
+ *   hidden  1 <= rows, cols <= 65536
+ *   aux     1 <= rows <= 2^24, 1 <= cols <= 65536, rows * cols < 2^31
+ *   vector  rows * cols elements form one vector; 1 <= rows * cols < 2^31
  */
 typedef struct {
   int64_t rows;
@@ -92,16 +115,23 @@ typedef struct {
 typedef struct meq_plan meq_plan; /* opaque; owns host metadata only */
 
 /* Fill *hp with the paper's defaults: mu 0.95, rho 0.2, lambda 0.1, K 5,
- * (a, b, c) = (3.4445, -4.7750, 2.0315), delta 1e-7, nesterov 0.  No-op on null. */
+ * (a, b, c) = (3.4445, -4.7750, 2.0315), delta 1e-7, nesterov 0,
+ * update_rule MEQ_RULE_MEQMUON.  No-op on null. */
 void meq_default_hparams(meq_hparams* hp);
 
 /*
- * Validate `count` matrix descriptors and the hyperparameters and build a plan:
- * the matrices are grouped by shape for batched Newton-Schulz launches and the
- * workspace layout is fixed.  Touches no device and may run without a GPU.
- * count == 0 is allowed (meq_step is then a no-op).  On success *out receives a
- * plan the caller releases with meq_destroy; on failure *out is set to NULL.
+ * Validate `count` parameter descriptors of one meq_param_kind and the
+ * hyperparameters and build a plan: hidden matrices are grouped by shape for
+ * batched Newton-Schulz launches, and the workspace layout is fixed.  Touches no
+ * device and may run without a GPU.  count == 0 is allowed (meq_step is then a
+ * no-op).  On success *out receives a plan the caller releases with meq_destroy;
+ * on failure *out is set to NULL.  An unknown kind, or MEQ_RULE_MOONLIGHT with a
+ * kind other than MEQ_PARAM_HIDDEN, is MEQ_ERR_INVALID_ARG.
  */
+meq_status meq_init_kind(int32_t kind, const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp,
+                         meq_plan** out);
+
+/* meq_init_kind(MEQ_PARAM_HIDDEN, ...). */
 meq_status meq_init(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out);
 
 /* Bytes of device workspace meq_step needs for this plan (0 for a null plan). */
@@ -132,7 +162,8 @@ meq_status meq_step(meq_plan* plan, void* const* params, const void* const* grad
  * Copy the last step's per-matrix statistics from the workspace to host arrays
  * of `count` entries (any of them may be null): gamma_r, gamma_c are the row
  * and column CVs of U (eq. "cv", computed in double precision), dir the chosen
- * meq_direction.  Synchronizes with `stream`.
+ * meq_direction.  Synchronizes with `stream`.  Only hidden plans with
+ * MEQ_RULE_MEQMUON compute these; other plans return MEQ_ERR_UNSUPPORTED.
  */
 meq_status meq_get_stats(const meq_plan* plan, const void* workspace, double* gamma_r, double* gamma_c,
                          int32_t* dir, hipStream_t stream);
@@ -147,14 +178,18 @@ const char* meq_status_string(meq_status s);
  * Introspection (host only, no device work)
  * ------------------------------------------------------------------------- */
 
-/* Number of Newton-Schulz shape groups (matrices with equal (min, max) dims). */
+/* Number of Newton-Schulz shape groups (matrices with equal (min, max) dims);
+ * 0 for aux and vector plans. */
 int32_t meq_plan_num_groups(const meq_plan* plan);
 
 /* Shape group g: short side s, long side l (after transposing tall matrices to
  * wide orientation) and its number of matrices. */
 meq_status meq_plan_group(const meq_plan* plan, int32_t g, int64_t* s, int64_t* l, int32_t* count);
 
-/* Buffers of the workspace that tests may inspect after a step. */
+/* Buffers of the workspace that tests may inspect after a step.
+ * Hidden plans: all six.  Aux plans: MEQ_BUF_ROW_RMS (r of V), MEQ_BUF_COL_RMS
+ * (c of N_r(V)).  Vector plans: MEQ_BUF_NORMSQ (||V||_2^2).  Other pairs are
+ * MEQ_ERR_INVALID_ARG. */
 typedef enum {
   MEQ_BUF_X0 = 0,      /* bf16 V (not yet divided by ||V||_F), wide orientation s x l, ld = padded l;
                           still intact after a step only when ns_steps == 1 (later Newton-Schulz
@@ -163,7 +198,8 @@ typedef enum {
   MEQ_BUF_NORMSQ = 2,  /* double ||V||_F^2, 1 x 1                                                    */
   MEQ_BUF_ROW_RMS = 3, /* double r of U in the matrix's own orientation, 1 x rows                      */
   MEQ_BUF_COL_RMS = 4, /* double c of U in the matrix's own orientation, 1 x cols                      */
-  MEQ_BUF_SCALE = 5    /* float per-row (dir row, 1 x rows) or per-column (1 x cols) scale of U~ = U*s */
+  MEQ_BUF_SCALE = 5    /* float per-row (dir row, 1 x rows) or per-column (1 x cols) scale of U~ = U*s;
+                          with MEQ_RULE_MOONLIGHT every row's entry is sqrt(max(m, n))              */
 } meq_buffer_kind;
 
 /*
@@ -188,7 +224,11 @@ typedef enum {
   MEQ_K_ROWCOL = 5,   /* row and column sums of squares of U                                    */
   MEQ_K_SELECT = 6,   /* CVs, direction, scale vector                                           */
   MEQ_K_UPDATE = 7,   /* decoupled weight decay + normalized update write-back                   */
-  MEQ_K_COUNT = 8
+  MEQ_K_AUX_ROWS = 8,   /* aux: momentum + row RMS of V                                         */
+  MEQ_K_AUX_COLS = 9,   /* aux: column RMS of N_r(V) (partials + finalization)                   */
+  MEQ_K_AUX_UPDATE = 10, /* aux: decoupled weight decay + two-sided normalized update            */
+  MEQ_K_VECTOR = 11,    /* vector: momentum, global RMS and write-back in one kernel             */
+  MEQ_K_COUNT = 12
 } meq_kernel_kind;
 
 /* Bracket every launch of the kinds in `kind_mask` (bit k = meq_kernel_kind k)

@@ -25,6 +25,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", f"-I{INCLUDE}"
 SOURCES = {
     "k_ns_gemm.hip": [],
     "k_stream.hip": [],
+    "k_aux.hip": [],
     "meq_api.cpp": [],
 }
 
@@ -53,7 +54,8 @@ def build(verbose: bool = False) -> str:
                 raise RuntimeError(f"hipcc failed on {src}:\n{res.stdout or ''}")
             objs.append(obj)
         out_tmp = LIB + ".tmp"
-        cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", out_tmp]
+        # -z defs: an entry point whose kernel source is missing fails here, not at load time
+        cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,-z,defs", *objs, "-o", out_tmp]
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True)

@@ -1,6 +1,7 @@
 // Host side of the MeqMuon C ABI: argument validation, shape grouping, the
-// workspace layout, and the launch sequence of one step (Algorithm "MeqMuon",
-// hidden-weight branch).  meq_init touches no device; meq_step only enqueues.
+// workspace layout, and the launch sequence of one step for each parameter kind
+// (the three branches of Algorithm "MeqMuon", and the Moonlight-Muon rule for hidden
+// weights).  meq_init_kind touches no device; meq_step only enqueues.
 #include <algorithm>
 #include <cmath>
 #include <cstring>
@@ -20,6 +21,8 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int64_t kMaxDim = 65536;
+constexpr int64_t kMaxAuxRows = int64_t{1} << 24;
+constexpr int64_t kMaxElems = (int64_t{1} << 31) - 1;
 // Every per-matrix wide buffer must stay addressable with 32-bit byte offsets.
 constexpr int64_t kMaxWideBytes = (int64_t{1} << 31) - 1;
 
@@ -34,6 +37,10 @@ struct MatInfo {
   int tiles_pad_r, tiles_pad_c;  // 64x64 tiles over the padded matrix in its own orientation
   int tiles_upd_r, tiles_upd_c;  // 64x64 tiles over the real matrix
   size_t off_part, off_rrms, off_crms, off_scale;
+  // aux and vector plans
+  int row_blocks;
+  int64_t len;
+  size_t off_rscale, off_cscale, off_cpart, off_normsq;
 };
 
 struct GroupInfo {
@@ -51,6 +58,7 @@ struct TimedLaunch {
 }  // namespace
 
 struct meq_plan {
+  int kind = MEQ_PARAM_HIDDEN;
   meq_hparams hp;
   std::vector<MatInfo> mats;
   std::vector<GroupInfo> groups;
@@ -75,8 +83,20 @@ meq_status validate_hparams(const meq_hparams& hp) {
   if (!finite(hp.ns_a) || !finite(hp.ns_b) || !finite(hp.ns_c)) return MEQ_ERR_INVALID_ARG;
   if (!finite(hp.zero_rms_delta) || hp.zero_rms_delta < 0.f) return MEQ_ERR_INVALID_ARG;
   if (hp.nesterov != 0 && hp.nesterov != 1) return MEQ_ERR_INVALID_ARG;
+  if (hp.update_rule != MEQ_RULE_MEQMUON && hp.update_rule != MEQ_RULE_MOONLIGHT) return MEQ_ERR_INVALID_ARG;
   return MEQ_OK;
 }
+
+// (param, grad) dtypes: both known, and equal.
+meq_status validate_dtypes(const meq_matrix_desc& d) {
+  const bool known = (d.param_dtype == MEQ_F32 || d.param_dtype == MEQ_BF16) &&
+                     (d.grad_dtype == MEQ_F32 || d.grad_dtype == MEQ_BF16);
+  if (!known) return MEQ_ERR_INVALID_ARG;
+  if (d.param_dtype != d.grad_dtype) return MEQ_ERR_UNSUPPORTED;
+  return MEQ_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 hipEvent_t take_event(meq_plan* p) {
   if (!p->event_pool.empty()) {
@@ -128,6 +148,7 @@ MEQ_EXPORT void meq_default_hparams(meq_hparams* hp) {
   hp->ns_c = 2.0315f;
   hp->zero_rms_delta = 1e-7f;
   hp->nesterov = 0;
+  hp->update_rule = MEQ_RULE_MEQMUON;
 }
 
 MEQ_EXPORT const char* meq_status_string(meq_status s) {
@@ -141,17 +162,14 @@ MEQ_EXPORT const char* meq_status_string(meq_status s) {
   return "unknown status";
 }
 
-MEQ_EXPORT meq_status meq_init(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out) {
-  if (out) *out = nullptr;
-  if (!out || !hp || count < 0 || (count > 0 && !mats)) return MEQ_ERR_INVALID_ARG;
-  MEQ_TRY(validate_hparams(*hp));
+namespace {
+
+// Hidden 2D weights: shape groups for the Newton-Schulz launches and the workspace layout.
+meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out) {
   for (int i = 0; i < count; ++i) {
     const meq_matrix_desc& d = mats[i];
     if (d.rows < 1 || d.cols < 1 || d.rows > kMaxDim || d.cols > kMaxDim) return MEQ_ERR_INVALID_ARG;
-    const bool known = (d.param_dtype == MEQ_F32 || d.param_dtype == MEQ_BF16) &&
-                       (d.grad_dtype == MEQ_F32 || d.grad_dtype == MEQ_BF16);
-    if (!known) return MEQ_ERR_INVALID_ARG;
-    if (d.param_dtype != d.grad_dtype) return MEQ_ERR_UNSUPPORTED;
+    MEQ_TRY(validate_dtypes(d));
     const int64_t S = round_up(std::min(d.rows, d.cols), kTile), L = round_up(std::max(d.rows, d.cols), kTile);
     if (S * L * 2 > kMaxWideBytes) return MEQ_ERR_UNSUPPORTED;
   }
@@ -231,6 +249,69 @@ MEQ_EXPORT meq_status meq_init(const meq_matrix_desc* mats, int32_t count, const
   return MEQ_OK;
 }
 
+// Remaining 2D parameters (eq. "aux") and 1-D parameters (eq. "vector"): per-parameter
+// vectors and partials only.
+meq_status init_stream_kind(int32_t kind, const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp,
+                            meq_plan** out) {
+  for (int i = 0; i < count; ++i) {
+    const meq_matrix_desc& d = mats[i];
+    if (d.rows < 1 || d.cols < 1 || d.rows > kMaxElems || d.cols > kMaxElems) return MEQ_ERR_INVALID_ARG;
+    if (d.rows * d.cols > kMaxElems) return MEQ_ERR_UNSUPPORTED;
+    if (kind == MEQ_PARAM_AUX && (d.rows > kMaxAuxRows || d.cols > kMaxDim)) return MEQ_ERR_UNSUPPORTED;
+    MEQ_TRY(validate_dtypes(d));
+  }
+  meq_plan* p = new (std::nothrow) meq_plan();
+  if (!p) return MEQ_ERR_INVALID_ARG;
+  p->kind = kind;
+  p->hp = *hp;
+  p->mats.resize(count);
+  size_t off = 0;
+  for (int i = 0; i < count; ++i) {
+    MatInfo& mi = p->mats[i];
+    mi = MatInfo{};
+    mi.m = mats[i].rows;
+    mi.n = mats[i].cols;
+    mi.len = mi.m * mi.n;
+    mi.dtype = mats[i].param_dtype;
+    if (kind == MEQ_PARAM_AUX) {
+      mi.row_blocks = static_cast<int>((mi.m + kAuxColRows - 1) / kAuxColRows);
+      mi.off_rrms = off;
+      off = align_up(off + 8 * static_cast<size_t>(mi.m), kAlign);
+      mi.off_crms = off;
+      off = align_up(off + 8 * static_cast<size_t>(mi.n), kAlign);
+      mi.off_rscale = off;
+      off = align_up(off + 4 * static_cast<size_t>(mi.m), kAlign);
+      mi.off_cscale = off;
+      off = align_up(off + 4 * static_cast<size_t>(mi.n), kAlign);
+      mi.off_cpart = off;
+      off = align_up(off + 8 * static_cast<size_t>(mi.row_blocks) * mi.n, kAlign);
+    } else {
+      mi.off_normsq = off;
+      off = align_up(off + 8, kAlign);
+    }
+  }
+  p->ws_bytes = off;
+  *out = p;
+  return MEQ_OK;
+}
+
+}  // namespace
+
+MEQ_EXPORT meq_status meq_init_kind(int32_t kind, const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp,
+                                    meq_plan** out) {
+  if (out) *out = nullptr;
+  if (!out || !hp || count < 0 || (count > 0 && !mats)) return MEQ_ERR_INVALID_ARG;
+  if (kind != MEQ_PARAM_HIDDEN && kind != MEQ_PARAM_AUX && kind != MEQ_PARAM_VECTOR) return MEQ_ERR_INVALID_ARG;
+  MEQ_TRY(validate_hparams(*hp));
+  if (hp->update_rule != MEQ_RULE_MEQMUON && kind != MEQ_PARAM_HIDDEN) return MEQ_ERR_INVALID_ARG;
+  if (kind == MEQ_PARAM_HIDDEN) return init_hidden(mats, count, hp, out);
+  return init_stream_kind(kind, mats, count, hp, out);
+}
+
+MEQ_EXPORT meq_status meq_init(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out) {
+  return meq_init_kind(MEQ_PARAM_HIDDEN, mats, count, hp, out);
+}
+
 MEQ_EXPORT size_t meq_workspace_bytes(const meq_plan* plan) { return plan ? plan->ws_bytes : 0; }
 
 MEQ_EXPORT int32_t meq_plan_num_groups(const meq_plan* plan) {
@@ -250,9 +331,27 @@ MEQ_EXPORT meq_status meq_debug_region(const meq_plan* plan, int32_t matrix, int
                                        int64_t* rows, int64_t* cols, int64_t* ld) {
   if (!plan || matrix < 0 || matrix >= static_cast<int32_t>(plan->mats.size())) return MEQ_ERR_INVALID_ARG;
   const MatInfo& mi = plan->mats[matrix];
-  const GroupInfo& g = plan->groups[mi.group];
   size_t o = 0;
   int64_t r = 1, c = 1, d = 1;
+  if (plan->kind != MEQ_PARAM_HIDDEN) {
+    if (plan->kind == MEQ_PARAM_AUX && kind == MEQ_BUF_ROW_RMS) {
+      o = mi.off_rrms;
+      c = d = mi.m;
+    } else if (plan->kind == MEQ_PARAM_AUX && kind == MEQ_BUF_COL_RMS) {
+      o = mi.off_crms;
+      c = d = mi.n;
+    } else if (plan->kind == MEQ_PARAM_VECTOR && kind == MEQ_BUF_NORMSQ) {
+      o = mi.off_normsq;
+    } else {
+      return MEQ_ERR_INVALID_ARG;
+    }
+    if (offset) *offset = o;
+    if (rows) *rows = r;
+    if (cols) *cols = c;
+    if (ld) *ld = d;
+    return MEQ_OK;
+  }
+  const GroupInfo& g = plan->groups[mi.group];
   switch (kind) {
     case MEQ_BUF_X0:
     case MEQ_BUF_U: {
@@ -293,6 +392,85 @@ MEQ_EXPORT meq_status meq_debug_region(const meq_plan* plan, int32_t matrix, int
   return MEQ_OK;
 }
 
+namespace {
+
+float decay_of(const meq_hparams& hp, float lr) {
+  return static_cast<float>(1.0 - static_cast<double>(lr) * hp.weight_decay);
+}
+float step_of(const meq_hparams& hp, float lr) { return static_cast<float>(static_cast<double>(hp.rho) * lr); }
+
+// Remaining 2D parameters, one matrix at a time: rows (momentum + r), columns (c of
+// N_r(V)), write-back.
+meq_status step_aux(meq_plan* p, void* const* params, const void* const* grads, float* const* momenta, float lr,
+                    char* ws, hipStream_t st) {
+  const meq_hparams& hp = p->hp;
+  for (size_t i = 0; i < p->mats.size(); ++i) {
+    const MatInfo& mi = p->mats[i];
+    const bool bf = mi.dtype == MEQ_BF16;
+    AuxArgs a{};
+    a.m = static_cast<int>(mi.m);
+    a.n = static_cast<int>(mi.n);
+    a.nesterov = hp.nesterov;
+    a.row_blocks = mi.row_blocks;
+    a.mu = hp.mu;
+    a.decay = decay_of(hp, lr);
+    a.step = step_of(hp, lr);
+    a.delta = static_cast<double>(hp.zero_rms_delta);
+    a.g = grads[i];
+    a.b = momenta[i];
+    a.w = params[i];
+    const size_t ea = bf ? 8 : 16;  // four elements of the parameter / gradient dtype
+    a.vec = (mi.n % 4 == 0) && aligned(a.b, 16) && aligned(a.g, ea) && aligned(a.w, ea);
+    a.rrms = reinterpret_cast<double*>(ws + mi.off_rrms);
+    a.crms = reinterpret_cast<double*>(ws + mi.off_crms);
+    a.rscale = reinterpret_cast<float*>(ws + mi.off_rscale);
+    a.cscale = reinterpret_cast<float*>(ws + mi.off_cscale);
+    a.cpart = reinterpret_cast<double*>(ws + mi.off_cpart);
+    MEQ_TRY(timed_launch(p, MEQ_K_AUX_ROWS, st, [&] { return launch_aux_rows(a, bf, st); }));
+    MEQ_TRY(timed_launch(p, MEQ_K_AUX_COLS, st, [&] { return launch_aux_cols(a, bf, st); }));
+    MEQ_TRY(timed_launch(p, MEQ_K_AUX_COLS, st, [&] { return launch_aux_colfin(a, st); }));
+    MEQ_TRY(timed_launch(p, MEQ_K_AUX_UPDATE, st, [&] { return launch_aux_update(a, bf, st); }));
+  }
+  return MEQ_OK;
+}
+
+// 1-D parameters: one block per vector, up to kMaxChunk vectors of one dtype per launch.
+meq_status step_vec(meq_plan* p, void* const* params, const void* const* grads, float* const* momenta, float lr,
+                    char* ws, hipStream_t st) {
+  const meq_hparams& hp = p->hp;
+  const int count = static_cast<int>(p->mats.size());
+  for (int dt = 0; dt < 2; ++dt) {
+    VecArgs a{};
+    auto flush = [&]() -> meq_status {
+      if (a.count == 0) return MEQ_OK;
+      const VecArgs sent = a;
+      a.count = 0;
+      return timed_launch(p, MEQ_K_VECTOR, st, [&] { return launch_vec(sent, dt == MEQ_BF16, st); });
+    };
+    for (int i = 0; i < count; ++i) {
+      const MatInfo& mi = p->mats[i];
+      if (mi.dtype != dt) continue;
+      const int k = a.count++;
+      a.nesterov = hp.nesterov;
+      a.mu = hp.mu;
+      a.decay = decay_of(hp, lr);
+      a.step = step_of(hp, lr);
+      a.len[k] = mi.len;
+      a.g[k] = grads[i];
+      a.b[k] = momenta[i];
+      a.w[k] = params[i];
+      const size_t ea = dt == MEQ_BF16 ? 8 : 16;
+      a.vec[k] = (mi.len % 4 == 0) && aligned(a.b[k], 16) && aligned(a.g[k], ea) && aligned(a.w[k], ea);
+      a.normsq[k] = reinterpret_cast<double*>(ws + mi.off_normsq);
+      if (a.count == kMaxChunk) MEQ_TRY(flush());
+    }
+    MEQ_TRY(flush());
+  }
+  return MEQ_OK;
+}
+
+}  // namespace
+
 MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* const* grads, float* const* momenta,
                                float lr, void* workspace, size_t workspace_bytes, hipStream_t st) {
   if (!p) return MEQ_ERR_INVALID_ARG;
@@ -306,8 +484,11 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     return MEQ_ERR_WORKSPACE;
 
   char* ws = static_cast<char*>(workspace);
+  if (p->kind == MEQ_PARAM_AUX) return step_aux(p, params, grads, momenta, lr, ws, st);
+  if (p->kind == MEQ_PARAM_VECTOR) return step_vec(p, params, grads, momenta, lr, ws, st);
   MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
   const meq_hparams& hp = p->hp;
+  const bool moonlight = hp.update_rule == MEQ_RULE_MOONLIGHT;
 
   // Element-wise kernels run over chunks of matrices sharing a dtype.
   std::vector<std::vector<int>> chunks;
@@ -430,8 +611,8 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
       }
     }
   }
-  // 4. row / column sums of squares of U, per shape group
-  for (size_t gi = 0; gi < p->groups.size(); ++gi) {
+  // 4. row / column sums of squares of U, per shape group (MeqMuon only)
+  for (size_t gi = 0; gi < p->groups.size() && !moonlight; ++gi) {
     const GroupInfo& g = p->groups[gi];
     const int batch = static_cast<int>(g.mats.size());
     const int tm = static_cast<int>(g.S / kTile), tn = static_cast<int>(g.L / kTile);
@@ -450,7 +631,7 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     rc.tiles_c = tn;
     MEQ_TRY(timed_launch(p, MEQ_K_ROWCOL, st, [&] { return launch_rowcol(rc, batch, st); }));
   }
-  // 5. row/column RMS, CVs, direction, scale vectors
+  // 5. row/column RMS, CVs, direction, scale vectors (Moonlight: the uniform scale)
   for (int c0 = 0; c0 < count; c0 += kMaxChunk) {
     SelectArgs a{};
     a.count = std::min(kMaxChunk, count - c0);
@@ -471,8 +652,13 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
       a.scal[k] = scal + c0 + k;
       a.max_lines = std::max(a.max_lines, static_cast<int>(mi.s + mi.l));
     }
-    MEQ_TRY(timed_launch(p, MEQ_K_SELECT, st, [&] { return launch_rms(a, st); }));
-    MEQ_TRY(timed_launch(p, MEQ_K_SELECT, st, [&] { return launch_select(a, st); }));
+    if (moonlight) {
+      // U~ = sqrt(max(m, n)) U: one scale for every row, no statistics
+      MEQ_TRY(timed_launch(p, MEQ_K_SELECT, st, [&] { return launch_scale_fill(a, st); }));
+    } else {
+      MEQ_TRY(timed_launch(p, MEQ_K_SELECT, st, [&] { return launch_rms(a, st); }));
+      MEQ_TRY(timed_launch(p, MEQ_K_SELECT, st, [&] { return launch_select(a, st); }));
+    }
   }
   // 6. write-back
   const float decay = static_cast<float>(1.0 - static_cast<double>(lr) * hp.weight_decay);
@@ -509,6 +695,7 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
 MEQ_EXPORT meq_status meq_get_stats(const meq_plan* plan, const void* workspace, double* gamma_r, double* gamma_c,
                                     int32_t* dir, hipStream_t st) {
   if (!plan) return MEQ_ERR_INVALID_ARG;
+  if (plan->kind != MEQ_PARAM_HIDDEN || plan->hp.update_rule != MEQ_RULE_MEQMUON) return MEQ_ERR_UNSUPPORTED;
   const size_t count = plan->mats.size();
   if (count == 0) return MEQ_OK;
   if (!workspace) return MEQ_ERR_WORKSPACE;

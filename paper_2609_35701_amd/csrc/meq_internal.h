@@ -123,6 +123,39 @@ struct UpdateArgs {
   const MatScalars* scal[kMaxChunk];
 };
 
+// ------------------------------------------- remaining 2D parameters (eq. "aux"), one matrix per launch
+constexpr int kAuxRowsPerBlock = 4;  // row pass and write-back: one wave per row
+constexpr int kAuxColRows = 256;     // rows summed by one block of the column pass
+struct AuxArgs {
+  int m, n;
+  int nesterov;
+  int vec;         // n % 4 == 0: rows start 16-byte aligned (fp32) / 8-byte aligned (bf16)
+  int row_blocks;  // ceil(m / kAuxColRows)
+  float mu, decay, step;
+  double delta;
+  const void* g;
+  float* b;
+  void* w;
+  double* rrms;    // r of V, m entries
+  double* crms;    // c of N_r(V), n entries
+  float* rscale;   // 1 / r (0 at or below delta)
+  float* cscale;   // 1 / c (0 at or below delta)
+  double* cpart;   // row_blocks x n partial column sums of (V_ij / r_i)^2
+};
+
+// ------------------------------------------------------- 1-D parameters (eq. "vector")
+struct VecArgs {
+  int count;
+  int nesterov;
+  float mu, decay, step;
+  int64_t len[kMaxChunk];
+  int vec[kMaxChunk];  // length and pointers allow 4-element vector access
+  const void* g[kMaxChunk];
+  float* b[kMaxChunk];
+  void* w[kMaxChunk];
+  double* normsq[kMaxChunk];
+};
+
 // Launchers (defined in the .hip files).  Each returns the hipError_t of the launch.
 hipError_t launch_momentum(const MomentumArgs& a, int grad_bf16, int total_tiles, hipStream_t st);
 hipError_t launch_norm(const NormArgs& a, hipStream_t st);
@@ -131,5 +164,11 @@ hipError_t launch_rowcol(const RowColArgs& a, int batch, hipStream_t st);
 hipError_t launch_rms(const SelectArgs& a, hipStream_t st);
 hipError_t launch_select(const SelectArgs& a, hipStream_t st);
 hipError_t launch_update(const UpdateArgs& a, int param_bf16, int total_tiles, hipStream_t st);
+hipError_t launch_scale_fill(const SelectArgs& a, hipStream_t st);  // Moonlight: scale sqrt(max(m, n)), rows
+hipError_t launch_aux_rows(const AuxArgs& a, int grad_bf16, hipStream_t st);
+hipError_t launch_aux_cols(const AuxArgs& a, int grad_bf16, hipStream_t st);
+hipError_t launch_aux_colfin(const AuxArgs& a, hipStream_t st);
+hipError_t launch_aux_update(const AuxArgs& a, int bf16, hipStream_t st);
+hipError_t launch_vec(const VecArgs& a, int bf16, hipStream_t st);
 
 }  // namespace meq

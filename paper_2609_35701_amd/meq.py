@@ -1,4 +1,4 @@
-"""ctypes binding of libmeq.so (the MeqMuon hidden-weight update on MI355X).
+"""ctypes binding of libmeq.so (the MeqMuon optimizer update on MI355X).
 
 Argument marshalling only: every step of the update runs in the library's HIP
 kernels.  The names follow the C ABI in ``include/meq.h``.  If the library has
@@ -16,12 +16,16 @@ LIB_PATH = os.path.join(HERE, "libmeq.so")
 MEQ_OK, MEQ_ERR_INVALID_ARG, MEQ_ERR_UNSUPPORTED, MEQ_ERR_HIP, MEQ_ERR_WORKSPACE = 0, -1, -2, -3, -4
 MEQ_F32, MEQ_BF16 = 0, 1
 MEQ_DIR_ROW, MEQ_DIR_COL = 0, 1
+PARAM_HIDDEN, PARAM_AUX, PARAM_VECTOR = 0, 1, 2
+RULE_MEQMUON, RULE_MOONLIGHT = 0, 1
 BUF_X0, BUF_U, BUF_NORMSQ, BUF_ROW_RMS, BUF_COL_RMS, BUF_SCALE = range(6)
-(K_MOMENTUM, K_NORM, K_GRAM, K_POLY, K_APPLY, K_ROWCOL, K_SELECT, K_UPDATE) = range(8)
-KERNEL_NAMES = ("momentum", "norm", "gram", "poly", "apply", "rowcol", "select", "update")
+(K_MOMENTUM, K_NORM, K_GRAM, K_POLY, K_APPLY, K_ROWCOL, K_SELECT, K_UPDATE,
+ K_AUX_ROWS, K_AUX_COLS, K_AUX_UPDATE, K_VECTOR) = range(12)
+KERNEL_NAMES = ("momentum", "norm", "gram", "poly", "apply", "rowcol", "select", "update",
+                "aux_rows", "aux_cols", "aux_update", "vector")
 
-EXPORTED = ("meq_default_hparams", "meq_init", "meq_workspace_bytes", "meq_step", "meq_get_stats",
-            "meq_destroy", "meq_status_string", "meq_plan_num_groups", "meq_plan_group",
+EXPORTED = ("meq_default_hparams", "meq_init", "meq_init_kind", "meq_workspace_bytes", "meq_step",
+            "meq_get_stats", "meq_destroy", "meq_status_string", "meq_plan_num_groups", "meq_plan_group",
             "meq_debug_region", "meq_set_timing", "meq_get_timing")
 
 
@@ -38,7 +42,8 @@ class MeqError(RuntimeError):
 class HParams(ctypes.Structure):
     _fields_ = [("mu", ctypes.c_float), ("rho", ctypes.c_float), ("weight_decay", ctypes.c_float),
                 ("ns_steps", ctypes.c_int32), ("ns_a", ctypes.c_float), ("ns_b", ctypes.c_float),
-                ("ns_c", ctypes.c_float), ("zero_rms_delta", ctypes.c_float), ("nesterov", ctypes.c_int32)]
+                ("ns_c", ctypes.c_float), ("zero_rms_delta", ctypes.c_float), ("nesterov", ctypes.c_int32),
+                ("update_rule", ctypes.c_int32)]
 
 
 class MatrixDesc(ctypes.Structure):
@@ -61,6 +66,8 @@ def lib() -> ctypes.CDLL:
     L.meq_default_hparams.restype = None
     L.meq_init.argtypes = [ctypes.POINTER(MatrixDesc), c_i32, ctypes.POINTER(HParams), ctypes.POINTER(vp)]
     L.meq_init.restype = c_i32
+    L.meq_init_kind.argtypes = [c_i32, ctypes.POINTER(MatrixDesc), c_i32, ctypes.POINTER(HParams), ctypes.POINTER(vp)]
+    L.meq_init_kind.restype = c_i32
     L.meq_workspace_bytes.argtypes = [vp]
     L.meq_workspace_bytes.restype = c_sz
     L.meq_step.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.c_float, vp,
@@ -117,12 +124,16 @@ def _dtype_code(dtype) -> int:
 
 
 class Plan:
-    """A validated set of matrices plus hyperparameters (``meq_init``)."""
+    """A validated set of parameters of one kind plus hyperparameters (``meq_init_kind``).
 
-    def __init__(self, shapes: Sequence[Tuple[int, int]], param_dtype="bf16", grad_dtype=None,
-                 hparams: Optional[HParams] = None):
+    ``kind`` is PARAM_HIDDEN (2D hidden weights), PARAM_AUX (remaining 2D parameters)
+    or PARAM_VECTOR (1-D parameters; a shape (1, d) or (d,) each)."""
+
+    def __init__(self, shapes: Sequence[Tuple[int, ...]], param_dtype="bf16", grad_dtype=None,
+                 hparams: Optional[HParams] = None, kind: int = PARAM_HIDDEN):
         L = lib()
-        self.shapes = [(int(r), int(c)) for r, c in shapes]
+        self.kind = int(kind)
+        self.shapes = [(1, int(sh[0])) if len(sh) == 1 else (int(sh[0]), int(sh[1])) for sh in shapes]
         pd = _dtype_code(param_dtype)
         gd = pd if grad_dtype is None else _dtype_code(grad_dtype)
         n = len(self.shapes)
@@ -131,7 +142,8 @@ class Plan:
             descs[i] = MatrixDesc(r, c, pd, gd)
         self.hparams = hparams if hparams is not None else default_hparams()
         handle = ctypes.c_void_p()
-        _check(L.meq_init(descs, n, ctypes.byref(self.hparams), ctypes.byref(handle)), "meq_init")
+        _check(L.meq_init_kind(self.kind, descs, n, ctypes.byref(self.hparams), ctypes.byref(handle)),
+               "meq_init_kind")
         self._h = handle
         self.count = n
 
@@ -196,25 +208,33 @@ class Plan:
         return ms.value, n.value
 
 
-class HiddenWeightUpdate:
-    """Torch glue: owns fp32 momenta and the workspace for a list of 2D weights.
+class ParamUpdate:
+    """Torch glue: owns fp32 momenta and the workspace for a list of parameters of one kind.
 
-    ``step(grads, lr)`` enqueues one MeqMuon update of every weight on the
-    current torch stream.
+    ``step(grads, lr)`` enqueues one MeqMuon update of every parameter on the
+    current torch stream.  Hidden and aux parameters are 2D tensors; vector
+    parameters are 1-D (or any shape, taken as one flat vector).
     """
 
-    def __init__(self, params, hparams: Optional[HParams] = None):
+    kind = PARAM_HIDDEN
+
+    def __init__(self, params, hparams: Optional[HParams] = None, kind: Optional[int] = None):
         import torch
 
+        if kind is not None:
+            self.kind = int(kind)
         self.params = list(params)
         if not self.params:
             raise ValueError("no parameters")
         dev = self.params[0].device
         pdt = self.params[0].dtype
         for p in self.params:
-            if p.dim() != 2 or not p.is_contiguous() or p.device != dev or p.dtype != pdt:
-                raise ValueError("parameters must be contiguous 2D tensors of one dtype on one device")
-        self.plan = Plan([tuple(p.shape) for p in self.params], str(pdt), hparams=hparams)
+            if not p.is_contiguous() or p.device != dev or p.dtype != pdt:
+                raise ValueError("parameters must be contiguous tensors of one dtype on one device")
+            if self.kind != PARAM_VECTOR and p.dim() != 2:
+                raise ValueError("hidden and aux parameters must be 2D")
+        shapes = [tuple(p.shape) if self.kind != PARAM_VECTOR else (p.numel(),) for p in self.params]
+        self.plan = Plan(shapes, str(pdt), hparams=hparams, kind=self.kind)
         self.momenta = [torch.zeros(p.shape, dtype=torch.float32, device=dev) for p in self.params]
         self.workspace = torch.empty(max(self.plan.workspace_bytes, 256), dtype=torch.uint8, device=dev)
 
@@ -239,7 +259,7 @@ class HiddenWeightUpdate:
         return self.plan.stats_ptr(self.workspace.data_ptr(), st.cuda_stream)
 
     def view(self, matrix: int, kind: int):
-        """A torch view of a workspace buffer of one matrix (valid until the next step)."""
+        """A torch view of a workspace buffer of one parameter (valid until the next step)."""
         import torch
 
         off, rows, cols, ld = self.plan.debug_region(matrix, kind)
@@ -249,3 +269,22 @@ class HiddenWeightUpdate:
         if kind in (BUF_NORMSQ, BUF_ROW_RMS, BUF_COL_RMS):
             return self.workspace[off:off + 8 * cols].view(torch.float64)
         return self.workspace[off:off + 4 * cols].view(torch.float32)
+
+
+class HiddenWeightUpdate(ParamUpdate):
+    """2D hidden-layer weights: Newton-Schulz + adaptive one-sided normalization (or the
+    Moonlight-Muon rule with ``hparams.update_rule = RULE_MOONLIGHT``)."""
+
+    kind = PARAM_HIDDEN
+
+
+class AuxUpdate(ParamUpdate):
+    """Remaining 2D parameters (token embedding, LM head): two-sided normalization."""
+
+    kind = PARAM_AUX
+
+
+class VectorUpdate(ParamUpdate):
+    """1-D parameters (norm weights, biases): global-RMS normalization."""
+
+    kind = PARAM_VECTOR

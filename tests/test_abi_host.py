@@ -131,5 +131,104 @@ def test_debug_regions_and_timing_kinds():
         plan.debug_region(0, 99)
     plan.set_timing([meq.K_APPLY, meq.K_GRAM])
     assert plan.get_timing(meq.K_APPLY) == (0.0, 0)
+    assert plan.get_timing(meq.K_VECTOR) == (0.0, 0)
     with pytest.raises(meq.MeqError):
-        plan.get_timing(8)
+        plan.get_timing(len(meq.KERNEL_NAMES))
+
+
+# ------------------------------------------------------------------ parameter kinds
+def _init_kind(kind, descs, hp=None):
+    L = meq.lib()
+    arr = (meq.MatrixDesc * max(len(descs), 1))(*[meq.MatrixDesc(*d) for d in descs])
+    h = ctypes.c_void_p()
+    hp = hp or meq.default_hparams()
+    st = L.meq_init_kind(kind, arr, len(descs), ctypes.byref(hp), ctypes.byref(h))
+    if h.value:
+        L.meq_destroy(h)
+    return st
+
+
+BF = (meq.MEQ_BF16, meq.MEQ_BF16)
+F32 = (meq.MEQ_F32, meq.MEQ_F32)
+
+
+@pytest.mark.parametrize("kind,desc,status", [
+    (meq.PARAM_AUX, (32000, 2048, *BF), meq.MEQ_OK),
+    (meq.PARAM_AUX, (151936, 896, *BF), meq.MEQ_OK),          # a large-vocabulary embedding
+    (meq.PARAM_AUX, (7, 3, *F32), meq.MEQ_OK),
+    (meq.PARAM_AUX, (1 << 24, 8, *BF), meq.MEQ_OK),
+    ((meq.PARAM_AUX), ((1 << 24) + 1, 8, *BF), meq.MEQ_ERR_UNSUPPORTED),
+    (meq.PARAM_AUX, (8, 65537, *BF), meq.MEQ_ERR_UNSUPPORTED),
+    (meq.PARAM_AUX, (1 << 20, 4096, *BF), meq.MEQ_ERR_UNSUPPORTED),  # 2^32 elements
+    (meq.PARAM_AUX, (0, 8, *BF), meq.MEQ_ERR_INVALID_ARG),
+    (meq.PARAM_AUX, (8, 8, meq.MEQ_BF16, meq.MEQ_F32), meq.MEQ_ERR_UNSUPPORTED),
+    (meq.PARAM_VECTOR, (1, 2048, *BF), meq.MEQ_OK),
+    (meq.PARAM_VECTOR, (1, 1, *F32), meq.MEQ_OK),
+    (meq.PARAM_VECTOR, (3, 5, *F32), meq.MEQ_OK),              # any shape is one flat vector
+    (meq.PARAM_VECTOR, (1, (1 << 31) - 1, *F32), meq.MEQ_OK),
+    (meq.PARAM_VECTOR, (2, 1 << 30, *F32), meq.MEQ_ERR_UNSUPPORTED),
+    (meq.PARAM_VECTOR, (1, 0, *F32), meq.MEQ_ERR_INVALID_ARG),
+    (meq.PARAM_VECTOR, (1, 8, 5, meq.MEQ_F32), meq.MEQ_ERR_INVALID_ARG),
+])
+def test_init_kind_validates_descriptors(kind, desc, status):
+    assert _init_kind(kind, [desc]) == status
+
+
+def test_init_kind_rejects_unknown_kind_and_moonlight_outside_hidden():
+    assert _init_kind(3, [(4, 8, *BF)]) == meq.MEQ_ERR_INVALID_ARG
+    assert _init_kind(-1, [(4, 8, *BF)]) == meq.MEQ_ERR_INVALID_ARG
+    moon = meq.default_hparams(update_rule=meq.RULE_MOONLIGHT)
+    assert _init_kind(meq.PARAM_HIDDEN, [(4, 8, *BF)], moon) == meq.MEQ_OK
+    assert _init_kind(meq.PARAM_AUX, [(4, 8, *BF)], moon) == meq.MEQ_ERR_INVALID_ARG
+    assert _init_kind(meq.PARAM_VECTOR, [(1, 8, *BF)], moon) == meq.MEQ_ERR_INVALID_ARG
+    assert _init_kind(meq.PARAM_HIDDEN, [(4, 8, *BF)], meq.default_hparams(update_rule=2)) == \
+        meq.MEQ_ERR_INVALID_ARG
+    # meq_init is the hidden kind
+    assert _init([(4, 8, *BF)], moon) == meq.MEQ_OK
+
+
+def test_aux_and_vector_plans_layout_and_regions():
+    aux = meq.Plan([(32000, 2048), (300, 7)], "bf16", kind=meq.PARAM_AUX)
+    assert aux.groups() == []
+    # r, c (double), their reciprocals (float) and 256-row column partials (double)
+    want = 0
+    for m, n in [(32000, 2048), (300, 7)]:
+        for nbytes in (8 * m, 8 * n, 4 * m, 4 * n, 8 * ((m + 255) // 256) * n):
+            want += (nbytes + 255) // 256 * 256
+    assert aux.workspace_bytes == want
+    off_r, r, c, _ = aux.debug_region(1, meq.BUF_ROW_RMS)
+    off_c, r2, c2, _ = aux.debug_region(1, meq.BUF_COL_RMS)
+    assert (r, c, r2, c2) == (1, 300, 1, 7) and off_c > off_r
+    for k in (meq.BUF_X0, meq.BUF_U, meq.BUF_NORMSQ, meq.BUF_SCALE):
+        with pytest.raises(meq.MeqError):
+            aux.debug_region(0, k)
+    vec = meq.Plan([(2048,), (1, 5), (3, 4)], "f32", kind=meq.PARAM_VECTOR)
+    assert vec.workspace_bytes == 3 * 256
+    assert vec.debug_region(2, meq.BUF_NORMSQ)[0] == 512
+    with pytest.raises(meq.MeqError):
+        vec.debug_region(0, meq.BUF_ROW_RMS)
+
+
+def test_stats_only_for_meqmuon_hidden_plans():
+    L = meq.lib()
+    for plan in (meq.Plan([(4, 8)], "f32", kind=meq.PARAM_AUX), meq.Plan([(8,)], "f32", kind=meq.PARAM_VECTOR),
+                 meq.Plan([(4, 8)], "f32", hparams=meq.default_hparams(update_rule=meq.RULE_MOONLIGHT))):
+        st = L.meq_get_stats(plan.handle, ctypes.c_void_p(0x100000), None, None, None, None)
+        assert st == meq.MEQ_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("kind", [meq.PARAM_AUX, meq.PARAM_VECTOR])
+def test_kind_step_rejects_bad_arguments_before_any_device_work(kind):
+    plan = meq.Plan([(4, 8), (16, 3)], "f32", kind=kind)
+    L = meq.lib()
+    P = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    Z = (ctypes.c_void_p * 2)(0x1000, 0)
+    ws = plan.workspace_bytes
+
+    def step(params=P, grads=P, moms=P, lr=0.02, w=0x100000, wb=ws):
+        return L.meq_step(plan.handle, params, grads, moms, ctypes.c_float(lr), ctypes.c_void_p(w), wb, None)
+
+    assert step(moms=Z) == meq.MEQ_ERR_INVALID_ARG
+    assert step(lr=float("inf")) == meq.MEQ_ERR_INVALID_ARG
+    assert step(w=0) == meq.MEQ_ERR_WORKSPACE
+    assert step(wb=ws - 1) == meq.MEQ_ERR_WORKSPACE

@@ -1,0 +1,211 @@
+"""GPU parity of the other parameter kinds against the fp64 oracle, through the C ABI:
+remaining 2D parameters (two-sided normalization, eq. "aux"), 1-D parameters
+(global RMS, eq. "vector") and the Moonlight-Muon rule on the hidden path
+(eq. "moonlight-update").
+
+Each step is checked stage by stage on the GPU's own state (momentum, r, c or
+||V||^2, the written parameter) and the next step starts from the GPU's state, so
+per-step rounding does not accumulate into the comparison.  Tolerances: 1e-5
+relative for fp32 stages; bf16 parameters within one bf16 ulp of the oracle's
+rounded value plus the fp32 evaluation error, with at least 99.9% bit-exact;
+Newton-Schulz output and the Moonlight parameter delta within 3e-2.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from gpu_support import (TOL_DELTA, TOL_FP32, TOL_NS, log, oracle_hp, relerr, to_dev, to_np, ulp_bf16)
+from paper_2609_35701_amd import meq
+
+pytestmark = pytest.mark.gpu
+
+
+def f32(x: float) -> float:
+    """The float32 value the C boundary receives for a Python float (lr is a float argument)."""
+    return float(np.float32(x))
+
+
+def check_written(w_gpu, w_before, w_or, ut_or, lr, hp, dtype, label):
+    if dtype == "bf16":
+        w_rne = oracle.round_bf16(w_or)
+        off = np.abs(w_gpu - w_rne)
+        bound = ulp_bf16(w_rne) + 2.0 ** -21 * (np.abs(w_before) + hp.rho * lr * np.abs(ut_or))
+        bad = off > bound
+        assert not np.any(bad), f"{label}: {int(bad.sum())} bf16 entries beyond 1 ulp"
+        exact = float(np.mean(off == 0))
+        assert exact >= 0.999, f"{label}: only {exact:.5f} bit-exact"
+    else:
+        e = relerr(w_gpu - w_before, w_or - w_before)
+        assert e <= TOL_FP32, f"{label}: fp32 parameter delta {e}"
+
+
+# ------------------------------------------------------------------ eq. "aux"
+def run_aux(shape, dtype, steps, seed, hp=None, zero_rows=(), zero_cols=(), sigma=1.0, lr=0.02,
+            offset=0):
+    m, n = shape
+    log(f"aux {shape} {dtype} steps={steps} seed={seed} zero_rows={list(zero_rows)} zero_cols={list(zero_cols)} "
+        f"offset={offset}")
+    hp = hp or meq.default_hparams()
+    ohp = oracle_hp(hp)
+    wl = workloads.custom([shape], dtype, seed=seed, sigma=sigma)
+    w = workloads.weight_init(wl, 0).astype(np.float64)
+    if offset:
+        # a parameter that does not start on a 16-byte boundary takes the scalar path
+        flat = torch.zeros(m * n + offset, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32, device="cuda:0")
+        param = flat[offset:].view(m, n)
+        param.copy_(to_dev(w, dtype))
+    else:
+        param = to_dev(w, dtype)
+    upd = meq.AuxUpdate([param], hp)
+    b = np.zeros(shape)
+    for t in range(steps):
+        g = workloads.grad_at_step(wl, 0, t).astype(np.float64)
+        g[list(zero_rows), :] = 0.0
+        g[:, list(zero_cols)] = 0.0
+        upd.step([to_dev(g, dtype)], lr)
+        torch.cuda.synchronize()
+        out = oracle.aux_step(w, g, b, ohp, f32(lr))
+        label = f"aux {shape} {dtype} step {t}"
+        b_gpu = to_np(upd.momenta[0])
+        assert relerr(b_gpu, out["B"]) <= TOL_FP32, f"{label}: momentum"
+        r_gpu = to_np(upd.view(0, meq.BUF_ROW_RMS))
+        c_gpu = to_np(upd.view(0, meq.BUF_COL_RMS))
+        assert relerr(r_gpu, out["r"]) <= TOL_FP32, f"{label}: row RMS {relerr(r_gpu, out['r'])}"
+        assert relerr(c_gpu, out["c"]) <= TOL_FP32, f"{label}: column RMS {relerr(c_gpu, out['c'])}"
+        w_gpu = to_np(param)
+        check_written(w_gpu, w, out["W"], out["Ut"], f32(lr), ohp, dtype, label)
+        # a zero row gets only the decay: fma(decay, w, -0) rounded to fp32, then to bf16
+        decay32 = np.float32(1.0 - f32(lr) * f32(hp.weight_decay))
+        for i in zero_rows:
+            want = np.float32(np.float64(decay32) * w[i]).astype(np.float64)
+            if dtype == "bf16":
+                want = oracle.round_bf16(want)
+            np.testing.assert_array_equal(w_gpu[i], want, err_msg=f"{label}: zero row {i}")
+        w, b = w_gpu, b_gpu
+    return upd
+
+
+@pytest.mark.parametrize("shape,dtype", [((37, 53), "f32"), ((37, 53), "bf16"), ((300, 2048), "bf16"),
+                                         ((1000, 1001), "f32"), ((513, 64), "bf16"), ((1, 5), "f32"),
+                                         ((6, 1), "bf16")])
+def test_aux_parity_shapes(shape, dtype):
+    run_aux(shape, dtype, steps=3, seed=11)
+
+
+def test_aux_parity_nesterov():
+    run_aux((257, 96), "bf16", steps=3, seed=12, hp=meq.default_hparams(nesterov=1))
+    run_aux((33, 17), "f32", steps=2, seed=13, hp=meq.default_hparams(nesterov=1))
+
+
+def test_aux_parity_zero_rows_and_columns():
+    run_aux((64, 40), "f32", steps=2, seed=14, zero_rows=(3, 17), zero_cols=(0, 39))
+    run_aux((64, 40), "bf16", steps=2, seed=15, zero_rows=(5,), zero_cols=(12,))
+
+
+def test_aux_parity_misaligned_parameter():
+    run_aux((48, 64), "bf16", steps=2, seed=16, offset=1)
+    run_aux((48, 64), "f32", steps=2, seed=17, offset=3)
+
+
+def test_aux_parity_embedding_size():
+    # a Llama-1B token embedding at full size, strong row imbalance (sigma 1.5)
+    run_aux((32000, 2048), "bf16", steps=1, seed=18, sigma=1.5)
+
+
+# --------------------------------------------------------------- eq. "vector"
+def run_vec(lengths, dtype, steps, seed, hp=None, zero=(), lr=0.02, offset=0):
+    log(f"vector {len(lengths)} vectors {dtype} steps={steps} seed={seed} offset={offset}")
+    hp = hp or meq.default_hparams()
+    ohp = oracle_hp(hp)
+    wl = workloads.custom([(1, d) for d in lengths], dtype, seed=seed)
+    ws = [workloads.weight_init(wl, i).astype(np.float64).ravel() for i in range(len(lengths))]
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    if offset:
+        flat = torch.zeros(sum(lengths) + offset * len(lengths), dtype=tdt, device="cuda:0")
+        params, o = [], offset
+        for w in ws:
+            p = flat[o:o + w.size]
+            p.copy_(to_dev(w, dtype))
+            params.append(p)
+            o += w.size + offset
+    else:
+        params = [to_dev(w, dtype) for w in ws]
+    upd = meq.VectorUpdate(params, hp)
+    bs = [np.zeros(d) for d in lengths]
+    for t in range(steps):
+        gs = [workloads.grad_at_step(wl, i, t).astype(np.float64).ravel() for i in range(len(lengths))]
+        for i in zero:
+            gs[i][:] = 0.0
+        upd.step([to_dev(g, dtype) for g in gs], lr)
+        torch.cuda.synchronize()
+        for i, d in enumerate(lengths):
+            label = f"vector {i} (d={d}) {dtype} step {t}"
+            out = oracle.vec_step(ws[i], gs[i], bs[i], ohp, f32(lr))
+            b_gpu = to_np(upd.momenta[i])
+            assert relerr(b_gpu, out["B"]) <= TOL_FP32, f"{label}: momentum"
+            nsq = float(upd.view(i, meq.BUF_NORMSQ).cpu()[0])
+            assert abs(nsq - out["normsq"]) <= TOL_FP32 * max(out["normsq"], 1e-300), f"{label}: ||V||^2"
+            w_gpu = to_np(params[i])
+            check_written(w_gpu, ws[i], out["W"], out["Ut"], f32(lr), ohp, dtype, label)
+            ws[i], bs[i] = w_gpu, b_gpu
+
+
+def test_vector_parity_lengths():
+    lens = [1, 3, 4, 64, 2048, 4097, 100003]
+    run_vec(lens, "f32", steps=3, seed=21)
+    run_vec(lens, "bf16", steps=3, seed=22)
+
+
+def test_vector_parity_many_vectors_and_zero():
+    # 40 vectors span two launches (32 per launch); vector 5 has a zero gradient
+    lens = [2048] * 33 + [17, 1, 1000, 999, 2, 4096, 5]
+    run_vec(lens, "bf16", steps=2, seed=23, zero=(5,))
+
+
+def test_vector_parity_nesterov_and_misaligned():
+    run_vec([2048, 7, 1024], "f32", steps=3, seed=24, hp=meq.default_hparams(nesterov=1))
+    run_vec([2048, 8, 1024], "bf16", steps=2, seed=25, offset=1)
+
+
+# ----------------------------------------------------- eq. "moonlight-update"
+@pytest.mark.parametrize("shape,dtype", [((256, 512), "f32"), ((300, 100), "bf16"), ((768, 2048), "bf16"),
+                                         ((2048, 768), "bf16")])
+def test_moonlight_parity(shape, dtype):
+    m, n = shape
+    log(f"moonlight {shape} {dtype}")
+    hp = meq.default_hparams(update_rule=meq.RULE_MOONLIGHT)
+    ohp = oracle_hp(hp)
+    wl = workloads.custom([shape], dtype, seed=31)
+    w = workloads.weight_init(wl, 0).astype(np.float64)
+    param = to_dev(w, dtype)
+    upd = meq.HiddenWeightUpdate([param], hp)
+    b = np.zeros(shape)
+    lr = 0.02
+    for t in range(2):
+        g = workloads.grad_at_step(wl, 0, t).astype(np.float64)
+        upd.step([to_dev(g, dtype)], lr)
+        torch.cuda.synchronize()
+        label = f"moonlight {shape} {dtype} step {t}"
+        out = oracle.moonlight_step(w, g, b, ohp, f32(lr), wide=True)
+        b_gpu = to_np(upd.momenta[0])
+        assert relerr(b_gpu, out["B"]) <= TOL_FP32, f"{label}: momentum"
+        u_w = to_np(upd.view(0, meq.BUF_U))
+        u_gpu = u_w.T if m > n else u_w
+        e_ns = relerr(u_gpu, out["U"])
+        assert e_ns <= TOL_NS, f"{label}: NS {e_ns}"
+        sc = to_np(upd.view(0, meq.BUF_SCALE))[:m]
+        np.testing.assert_array_equal(sc, np.float32(math.sqrt(max(m, n))))
+        w_gpu = to_np(param)
+        # stage: the write-back of the GPU's own U
+        ut_stage = math.sqrt(max(m, n)) * u_gpu
+        w_stage = oracle.write_back(w, ut_stage, f32(lr), ohp.rho, ohp.weight_decay)
+        check_written(w_gpu, w, w_stage, ut_stage, f32(lr), ohp, dtype, label)
+        e_d = relerr(w_gpu - w, out["W"] - w)
+        assert e_d <= TOL_DELTA, f"{label}: parameter delta {e_d}"
+        with pytest.raises(meq.MeqError):
+            upd.stats()
+        w, b = w_gpu, b_gpu
