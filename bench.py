@@ -153,6 +153,75 @@ def stage_bytes(elems: int, param_bytes: int):
             "update": elems * (2 + 2 * param_bytes)}
 
 
+def time_steps(upd, grads, lr: float, steps: int, warmup: int, kinds) -> dict:
+    """Wall time per step and per-kind kernel time (HIP events on the launch stream)."""
+    import torch
+
+    from paper_2609_35701_amd import meq
+
+    for _ in range(warmup):
+        upd.step(grads, lr)
+    torch.cuda.synchronize()
+    upd.plan.set_timing(kinds)
+    for k in kinds:
+        upd.plan.get_timing(k, reset=True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        upd.step(grads, lr)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    out = {"ms_per_step": (t1 - t0) * 1e3 / steps}
+    for k in kinds:
+        ms, n = upd.plan.get_timing(k)
+        out[meq.KERNEL_NAMES[k] + "_ms"] = ms / steps
+    upd.plan.set_timing([])
+    return out
+
+
+def extras_leg(params, wl, lr: float, steps: int, warmup: int) -> dict:
+    """The other parameter kinds of the same 1B-shape model, and the Moonlight-Muon rule on its
+    hidden weights (same Newton-Schulz kernels, no equilibration)."""
+    import torch
+
+    from paper_2609_35701_amd import meq
+
+    dev = params[0].device
+    out = {}
+    # Moonlight-Muon on the same 112 hidden matrices: the difference to the MeqMuon step is the
+    # cost of the row/column statistics, CVs and direction choice
+    g_hidden = [torch.randn_like(p) * 1e-3 for p in params]
+    moon = meq.HiddenWeightUpdate(params, meq.default_hparams(update_rule=meq.RULE_MOONLIGHT))
+    out["moonlight_hidden"] = time_steps(moon, g_hidden, lr, steps, warmup,
+                                         [meq.K_ROWCOL, meq.K_SELECT, meq.K_UPDATE])
+    del moon, g_hidden
+    torch.cuda.empty_cache()
+    # remaining 2D parameters: the Llama token embedding and LM head (32000 x 2048, untied), bf16
+    aux_p = [torch.randn(32000, 2048, device=dev).mul_(0.02).to(torch.bfloat16) for _ in range(2)]
+    aux_g = [(torch.randn(32000, 2048, device=dev) * torch.rand(32000, 1, device=dev).mul_(3).exp_()
+              * 1e-4).to(torch.bfloat16) for _ in range(2)]
+    aux = meq.AuxUpdate(aux_p, meq.default_hparams())
+    t = time_steps(aux, aux_g, lr, steps, warmup, [meq.K_AUX_ROWS, meq.K_AUX_COLS, meq.K_AUX_UPDATE])
+    elems = sum(p.numel() for p in aux_p)
+    # bytes per element: rows (G 2, B 4 + 4), columns (B 4), write-back (B 4, W 2 + 2)
+    bytes_step = elems * (10 + 4 + 8)
+    kern_ms = t["aux_rows_ms"] + t["aux_cols_ms"] + t["aux_update_ms"]
+    t.update({"shapes": "2 x 32000x2048 bf16", "bytes_per_step": bytes_step,
+              "gbs": bytes_step / (kern_ms * 1e-3) / 1e9,
+              "roofline": {"bound": "hbm", "achieved": bytes_step / (kern_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
+                           "unit": "GB/s", "frac": bytes_step / (kern_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}})
+    out["aux_two_sided"] = t
+    del aux, aux_p, aux_g
+    # 1-D parameters: the 33 RMSNorm weights (2 per layer + final), bf16
+    vec_p = [torch.ones(2048, device=dev, dtype=torch.bfloat16) for _ in range(2 * 16 + 1)]
+    vec_g = [torch.randn(2048, device=dev).mul_(1e-3).to(torch.bfloat16) for _ in vec_p]
+    vec = meq.VectorUpdate(vec_p, meq.default_hparams())
+    t = time_steps(vec, vec_g, lr, steps, warmup, [meq.K_VECTOR])
+    t.update({"shapes": "33 x 2048 bf16", "launches_per_step": 2,
+              "note": "latency-bound: 67,584 elements in one or two launches"})
+    out["vector_global_rms"] = t
+    return out
+
+
 def cpu_baseline_leg(wl, lr: float, budget_s: float):
     """Time the fp64 oracle on one matrix of each distinct shape and scale to a whole step."""
     import numpy as np
@@ -200,6 +269,8 @@ def main() -> int:
     ap.add_argument("--workload", default="llama-1b")
     ap.add_argument("--lr", type=float, default=0.02)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the other parameter kinds and the Moonlight-Muon comparison")
     ap.add_argument("--cpu-budget", type=float, default=30.0, help="seconds of oracle work at most")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain copy kernel of known size (torch.neg over 256 MiB of fp32) before the "
@@ -269,7 +340,7 @@ def main() -> int:
         kern[name] = {"ms_per_step": ms / args.steps, "launches_per_step": n / args.steps,
                       "avg_launch_ms": ms / n if n else None}
     print(f"# bench: {ms_per_step:.3f} ms/step; " +
-          ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in kern.items()), file=sys.stderr, flush=True)
+          ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in kern.items() if v["launches_per_step"]), file=sys.stderr, flush=True)
 
     sym = apply = dense = 0
     for m in wl.matrices:
@@ -296,6 +367,11 @@ def main() -> int:
         "byte_stages_gbs": sum(sb.values()) / (sum(kern[k]["ms_per_step"] for k in ("momentum", "rowcol", "update"))
                                                * 1e-3) / 1e9,
     }
+    extras = None
+    if not args.no_extras and wl.name == "llama-1b":
+        print("# bench: other parameter kinds and the Moonlight-Muon rule", file=sys.stderr, flush=True)
+        extras = extras_leg(params, wl, args.lr, min(args.steps, 20), max(args.warmup, 1))
+        extras["equilibration_overhead_ms"] = ms_per_step - extras["moonlight_hidden"]["ms_per_step"]
     cpu = None
     if not args.no_cpu_baseline:
         print("# bench: timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
@@ -309,7 +385,8 @@ def main() -> int:
                    "ns_steps": hp.ns_steps, "ns_tflop_per_step_sym": sym / 1e12,
                    "ns_tflop_per_step_dense": dense / 1e12},
         "roofline": roofline, "cpu_baseline": cpu, "stages": stages,
-        "kernels_ms_per_step": {k: v["ms_per_step"] for k, v in kern.items()},
+        "kernels_ms_per_step": {k: v["ms_per_step"] for k, v in kern.items() if v["launches_per_step"]},
+        "extras": extras,
     }
     print(json.dumps(line), flush=True)
     return 0

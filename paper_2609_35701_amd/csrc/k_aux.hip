@@ -2,7 +2,7 @@
 // the Moonlight-Muon scale (eq. "moonlight-update").  All are HBM-bound.
 //   remaining 2D parameters, U~ = N_c(N_r(V))          eq. "aux"
 //     k_aux_rows    momentum B <- mu B + G, V, row RMS r of V and 1/r       (one wave per row)
-//     k_aux_cols    partial column sums of (V_ij / r_i)^2 over 256-row blocks
+//     k_aux_cols    partial column sums of (V_ij / r_i)^2 over 128-row blocks
 //     k_aux_colfin  column RMS c of N_r(V) and 1/c
 //     k_aux_update  W <- decay W - step V_ij / (r_i c_j)                    (one wave per row)
 //   1-D parameters, U~ = V / (||V|| / sqrt(d))          eq. "vector"
@@ -117,9 +117,11 @@ __global__ __launch_bounds__(256) void k_aux_rows(AuxArgs a) {
 }
 
 // --------------------------------------------------------------- eq. "aux", columns
-// Block (x, y): columns 1024 x .. 1024 x + 1023 (4 per thread), rows 256 y .. 256 y + 255.
+// Block (x, y): columns 1024 x .. 1024 x + 1023 (4 per thread), rows kAuxColRows y .. + kAuxColRows - 1,
+// eight rows' loads in flight per thread.
 template <bool kGradBf16>
 __global__ __launch_bounds__(256) void k_aux_cols(AuxArgs a) {
+  constexpr int U = 8;
   const int n = a.n;
   const int r0 = blockIdx.y * kAuxColRows;
   const int r1 = min(a.m, r0 + kAuxColRows);
@@ -128,18 +130,25 @@ __global__ __launch_bounds__(256) void k_aux_cols(AuxArgs a) {
   if (a.vec) {
     const int c = blockIdx.x * 1024 + 4 * threadIdx.x;
     if (c >= n) return;
-    for (int r = r0; r < r1; ++r) {
-      const float rs = a.rscale[r];
-      const int64_t off = static_cast<int64_t>(r) * n + c;
-      float b[4];
-      load4<false>(a.b, off, b);
-      float g[4] = {0.f, 0.f, 0.f, 0.f};
-      if (a.nesterov) load4<kGradBf16>(a.g, off, g);
+    for (int r = r0; r < r1; r += U) {
+      float b[U][4], g[U][4], rs[U];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float v = a.nesterov ? fmaf(mu, b[q], g[q]) : b[q];
-        const float x = v * rs;
-        acc[q] += static_cast<double>(x) * x;
+      for (int u = 0; u < U; ++u) {
+        const int rr = min(r + u, r1 - 1);  // rows past r1 are loaded again and not added
+        const int64_t off = static_cast<int64_t>(rr) * n + c;
+        load4<false>(a.b, off, b[u]);
+        if (a.nesterov) load4<kGradBf16>(a.g, off, g[u]);
+        rs[u] = a.rscale[rr];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (r + u >= r1) break;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float v = a.nesterov ? fmaf(mu, b[u][q], g[u][q]) : b[u][q];
+          const float x = v * rs[u];
+          acc[q] += static_cast<double>(x) * x;
+        }
       }
     }
 #pragma unroll
@@ -161,14 +170,23 @@ __global__ __launch_bounds__(256) void k_aux_cols(AuxArgs a) {
   }
 }
 
+// 64 columns per block; the four waves take every fourth row block and meet in LDS,
+// added in a fixed order.
 __global__ __launch_bounds__(256) void k_aux_colfin(AuxArgs a) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= a.n) return;
+  __shared__ double part[4][64];
+  const int jj = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + jj;
   double t = 0.0;
-  for (int k = 0; k < a.row_blocks; ++k) t += a.cpart[static_cast<int64_t>(k) * a.n + j];
-  const double c = sqrt(t / a.m);
-  a.crms[j] = c;
-  a.cscale[j] = c > a.delta ? static_cast<float>(1.0 / c) : 0.f;
+  if (j < a.n)
+    for (int k = w; k < a.row_blocks; k += 4) t += a.cpart[static_cast<int64_t>(k) * a.n + j];
+  part[w][jj] = t;
+  __syncthreads();
+  if (w == 0 && j < a.n) {
+    const double sum = (part[0][jj] + part[1][jj]) + (part[2][jj] + part[3][jj]);
+    const double c = sqrt(sum / a.m);
+    a.crms[j] = c;
+    a.cscale[j] = c > a.delta ? static_cast<float>(1.0 / c) : 0.f;
+  }
 }
 
 // ------------------------------------------------------------ eq. "aux", write-back
@@ -307,7 +325,7 @@ hipError_t launch_aux_cols(const AuxArgs& a, int grad_bf16, hipStream_t st) {
 }
 
 hipError_t launch_aux_colfin(const AuxArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_aux_colfin, dim3((a.n + 255) / 256), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(k_aux_colfin, dim3((a.n + 63) / 64), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -125,7 +125,7 @@ struct UpdateArgs {
 
 // ------------------------------------------- remaining 2D parameters (eq. "aux"), one matrix per launch
 constexpr int kAuxRowsPerBlock = 4;  // row pass and write-back: one wave per row
-constexpr int kAuxColRows = 256;     // rows summed by one block of the column pass
+constexpr int kAuxColRows = 128;     // rows summed by one block of the column pass
 struct AuxArgs {
   int m, n;
   int nesterov;

@@ -190,10 +190,10 @@ def test_init_kind_rejects_unknown_kind_and_moonlight_outside_hidden():
 def test_aux_and_vector_plans_layout_and_regions():
     aux = meq.Plan([(32000, 2048), (300, 7)], "bf16", kind=meq.PARAM_AUX)
     assert aux.groups() == []
-    # r, c (double), their reciprocals (float) and 256-row column partials (double)
+    # r, c (double), their reciprocals (float) and 128-row column partials (double)
     want = 0
     for m, n in [(32000, 2048), (300, 7)]:
-        for nbytes in (8 * m, 8 * n, 4 * m, 4 * n, 8 * ((m + 255) // 256) * n):
+        for nbytes in (8 * m, 8 * n, 4 * m, 4 * n, 8 * ((m + 127) // 128) * n):
             want += (nbytes + 255) // 256 * 256
     assert aux.workspace_bytes == want
     off_r, r, c, _ = aux.debug_region(1, meq.BUF_ROW_RMS)
