@@ -47,56 +47,77 @@ __device__ __forceinline__ int find_matrix(const int* tile_start, int count, int
   return mi;
 }
 
+// Eight consecutive floats of a bf16 or fp32 array (16- or 32-byte access).
+template <bool kBf16>
+__device__ __forceinline__ void load8(const void* p, int64_t i, float (&x)[8]) {
+  if (kBf16) {
+    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      x[2 * q] = bf16_to_f32(w[q] & 0xffffu);
+      x[2 * q + 1] = bf16_to_f32(w[q] >> 16);
+    }
+  } else {
+    const float4 lo = *reinterpret_cast<const float4*>(static_cast<const float*>(p) + i);
+    const float4 hi = *reinterpret_cast<const float4*>(static_cast<const float*>(p) + i + 4);
+    x[0] = lo.x; x[1] = lo.y; x[2] = lo.z; x[3] = lo.w;
+    x[4] = hi.x; x[5] = hi.y; x[6] = hi.z; x[7] = hi.w;
+  }
+}
+
+__device__ __forceinline__ uint4 pack_bf16x8(const uint16_t (&h)[8]) {
+  uint4 v;
+  v.x = h[0] | (static_cast<uint32_t>(h[1]) << 16);
+  v.y = h[2] | (static_cast<uint32_t>(h[3]) << 16);
+  v.z = h[4] | (static_cast<uint32_t>(h[5]) << 16);
+  v.w = h[6] | (static_cast<uint32_t>(h[7]) << 16);
+  return v;
+}
+
 // --------------------------------------------------------------------------------
 // Momentum B <- mu B + G, V = B (or G + mu B), per-tile sum of V^2, bf16 V written
 // into the zero-padded wide buffer (transposed through LDS for tall matrices).
-// One block = one 64 x 64 tile of the padded matrix in its own orientation;
-// thread (ty, tx) owns rows ty + 16 k (k < 4) and columns 4 tx .. 4 tx + 3.
+// One block = one 64 x 128 tile of the padded matrix in its own orientation;
+// thread (ty, tx) owns rows ty + 16 k (k < 4) and columns 8 tx .. 8 tx + 7.
 template <bool kGradBf16>
 __global__ __launch_bounds__(256) void k_momentum(MomentumArgs a) {
-  __shared__ uint16_t tr[kEwTile][kEwTile + 4];
+  __shared__ __attribute__((aligned(16))) uint16_t tr[kEwCols][kEwRows + 8];  // tall: [own column][own row]
   __shared__ float red[4];
   const int mi = find_matrix(a.tile_start, a.count, blockIdx.x);
   const int t = blockIdx.x - a.tile_start[mi];
   const int tcols = a.tiles_c[mi];
-  const int r0 = (t / tcols) * kEwTile, c0 = (t % tcols) * kEwTile;
+  const int r0 = (t / tcols) * kEwRows, c0 = (t % tcols) * kEwCols;
   const int m = a.m[mi], n = a.n[mi];
   const bool tall = a.tall[mi] != 0;
+  const bool vec = a.vec[mi] != 0;
   const int64_t ldx = a.ldx[mi];
   float* __restrict__ bp = a.b[mi];
   uint16_t* __restrict__ xp = a.x[mi];
   const float mu = a.mu;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  const bool vec = (n & 3) == 0;
   float ss = 0.f;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int row = r0 + ty + 16 * k;
-    const int col = c0 + 4 * tx;
-    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    const int col = c0 + 8 * tx;
+    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (row < m && col < n) {
       const int64_t off = static_cast<int64_t>(row) * n + col;
-      float g[4], b[4];
       if (vec) {
-        float4 bv = *reinterpret_cast<const float4*>(bp + off);
-        b[0] = bv.x; b[1] = bv.y; b[2] = bv.z; b[3] = bv.w;
-        if (kGradBf16) {
-          uint2 gv = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.g[mi]) + off);
-          g[0] = bf16_to_f32(gv.x & 0xffffu); g[1] = bf16_to_f32(gv.x >> 16);
-          g[2] = bf16_to_f32(gv.y & 0xffffu); g[3] = bf16_to_f32(gv.y >> 16);
-        } else {
-          float4 gv = *reinterpret_cast<const float4*>(static_cast<const float*>(a.g[mi]) + off);
-          g[0] = gv.x; g[1] = gv.y; g[2] = gv.z; g[3] = gv.w;
-        }
+        float g[8], b[8];
+        load8<kGradBf16>(a.g[mi], off, g);
+        load8<false>(bp, off, b);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < 8; ++q) {
           b[q] = fmaf(mu, b[q], g[q]);
           v[q] = a.nesterov ? fmaf(mu, b[q], g[q]) : b[q];
         }
         *reinterpret_cast<float4*>(bp + off) = make_float4(b[0], b[1], b[2], b[3]);
+        *reinterpret_cast<float4*>(bp + off + 4) = make_float4(b[4], b[5], b[6], b[7]);
       } else {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < 8; ++q) {
           if (col + q < n) {
             const float gq = kGradBf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.g[mi])[off + q])
                                        : static_cast<const float*>(a.g[mi])[off + q];
@@ -107,30 +128,28 @@ __global__ __launch_bounds__(256) void k_momentum(MomentumArgs a) {
         }
       }
     }
-    uint16_t h[4];
+    uint16_t h[8];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < 8; ++q) {
       ss = fmaf(v[q], v[q], ss);
       h[q] = f32_to_bf16(v[q]);
     }
     if (!tall) {
-      uint2 pk;
-      pk.x = h[0] | (static_cast<uint32_t>(h[1]) << 16);
-      pk.y = h[2] | (static_cast<uint32_t>(h[3]) << 16);
-      *reinterpret_cast<uint2*>(xp + static_cast<int64_t>(row) * ldx + col) = pk;
+      *reinterpret_cast<uint4*>(xp + static_cast<int64_t>(row) * ldx + col) = pack_bf16x8(h);
     } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) tr[4 * tx + q][ty + 16 * k] = h[q];
+      for (int q = 0; q < 8; ++q) tr[8 * tx + q][ty + 16 * k] = h[q];
     }
   }
   if (tall) {
     __syncthreads();
-    // wide row = own column, wide column = own row
+    // wide row = own column (128 of them), wide column = own row (64): 8 threads per wide row
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const int wr = ty + 16 * k;  // local own-column index
-      const uint2 pk = *reinterpret_cast<const uint2*>(&tr[wr][4 * tx]);
-      *reinterpret_cast<uint2*>(xp + static_cast<int64_t>(c0 + wr) * ldx + r0 + 4 * tx) = pk;
+      const int wr = (threadIdx.x >> 3) + 32 * k;  // local own-column index
+      const int wc = 8 * (threadIdx.x & 7);        // local own-row index
+      const uint4 pk = *reinterpret_cast<const uint4*>(&tr[wr][wc]);
+      *reinterpret_cast<uint4*>(xp + static_cast<int64_t>(c0 + wr) * ldx + r0 + wc) = pk;
     }
   }
   const float tot = block_sum256(ss, red);
@@ -169,22 +188,28 @@ __global__ __launch_bounds__(256) void k_rowcol(RowColArgs a) {
   const int r0 = ti * kTile, c0 = tj * kTile;
   float csum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   float* rp = a.rpart + mat * a.stride_rpart + static_cast<int64_t>(tj) * a.S + r0;
-  for (int q = 0; q < 32; ++q) {
-    const int r = rg + 8 * q;
-    const uint4 v = *reinterpret_cast<const uint4*>(u + static_cast<int64_t>(r0 + r) * a.L + c0 + 8 * cg);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    float rs = 0.f;
+  for (int q0 = 0; q0 < 32; q0 += 8) {
+    uint4 vv[8];  // eight rows' loads in flight
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const float lo = bf16_to_f32(w[p] & 0xffffu), hi = bf16_to_f32(w[p] >> 16);
-      csum[2 * p] = fmaf(lo, lo, csum[2 * p]);
-      csum[2 * p + 1] = fmaf(hi, hi, csum[2 * p + 1]);
-      rs = fmaf(lo, lo, rs);
-      rs = fmaf(hi, hi, rs);
+    for (int d = 0; d < 8; ++d)
+      vv[d] = *reinterpret_cast<const uint4*>(u + static_cast<int64_t>(r0 + rg + 8 * (q0 + d)) * a.L + c0 + 8 * cg);
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      const int r = rg + 8 * (q0 + d);
+      const uint32_t w[4] = {vv[d].x, vv[d].y, vv[d].z, vv[d].w};
+      float rs = 0.f;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const float lo = bf16_to_f32(w[p] & 0xffffu), hi = bf16_to_f32(w[p] >> 16);
+        csum[2 * p] = fmaf(lo, lo, csum[2 * p]);
+        csum[2 * p + 1] = fmaf(hi, hi, csum[2 * p + 1]);
+        rs = fmaf(lo, lo, rs);
+        rs = fmaf(hi, hi, rs);
+      }
+#pragma unroll
+      for (int off = 16; off > 0; off >>= 1) rs += __shfl_xor(rs, off, 64);
+      if (cg == 0) rp[r] = rs;
     }
-#pragma unroll
-    for (int off = 16; off > 0; off >>= 1) rs += __shfl_xor(rs, off, 64);
-    if (cg == 0) rp[r] = rs;
   }
 #pragma unroll
   for (int p = 0; p < 8; ++p) csh[rg][8 * cg + p] = csum[p];
@@ -269,88 +294,98 @@ __global__ __launch_bounds__(256) void k_select(SelectArgs a) {
 }
 
 // --------------------------------------------------------------------------------
-// W <- decay * W - step * U * scale  over 64 x 64 tiles of the matrix's own
-// orientation; U is read from the wide buffer (through LDS for tall matrices).
+// W <- decay * W - step * U * scale over 64 x 128 tiles of the matrix's own orientation
+// (thread (ty, tx): rows ty + 16 k, columns 8 tx .. 8 tx + 7); U is read from the padded
+// wide buffer (staged through LDS and transposed for tall matrices).
 template <bool kParamBf16>
 __global__ __launch_bounds__(256) void k_update(UpdateArgs a) {
-  __shared__ uint16_t tr[kEwTile][kEwTile + 4];
+  __shared__ __attribute__((aligned(16))) uint16_t tr[kEwCols][kEwRows + 8];  // tall: [own column][own row]
   const int mi = find_matrix(a.tile_start, a.count, blockIdx.x);
   const int t = blockIdx.x - a.tile_start[mi];
   const int tcols = a.tiles_c[mi];
-  const int r0 = (t / tcols) * kEwTile, c0 = (t % tcols) * kEwTile;
+  const int r0 = (t / tcols) * kEwRows, c0 = (t % tcols) * kEwCols;
   const int m = a.m[mi], n = a.n[mi];
   const bool tall = a.tall[mi] != 0;
+  const bool vec = a.vec[mi] != 0;
   const int64_t ldu = a.ldu[mi];
   const uint16_t* __restrict__ u = a.u[mi];
   const float* __restrict__ scale = a.scale[mi];
   const int dir = a.scal[mi]->dir;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   if (tall) {
-    // own tile rows r0.., cols c0.. = wide rows c0.., wide cols r0..  (wide buffer is padded: no bounds)
+    // own rows r0.., cols c0.. = wide rows c0.., wide cols r0..  (the wide buffer is padded: no bounds)
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const int wr = ty + 16 * k;
-      const uint2 pk = *reinterpret_cast<const uint2*>(u + static_cast<int64_t>(c0 + wr) * ldu + r0 + 4 * tx);
-      *reinterpret_cast<uint2*>(&tr[wr][4 * tx]) = pk;
+      const int wr = (threadIdx.x >> 3) + 32 * k;
+      const int wc = 8 * (threadIdx.x & 7);
+      const uint4 pk = *reinterpret_cast<const uint4*>(u + static_cast<int64_t>(c0 + wr) * ldu + r0 + wc);
+      *reinterpret_cast<uint4*>(&tr[wr][wc]) = pk;
     }
     __syncthreads();
   }
-  const bool vec = (n & 3) == 0;
   const float decay = a.decay, step = a.step;
+  // column scales: the same 8 for all four rows of this thread
+  const int col = c0 + 8 * tx;
+  float cs[8];
+  if (dir != 0) {
+    if (col + 8 <= n) {
+      const float4 lo = *reinterpret_cast<const float4*>(scale + col);
+      const float4 hi = *reinterpret_cast<const float4*>(scale + col + 4);
+      cs[0] = lo.x; cs[1] = lo.y; cs[2] = lo.z; cs[3] = lo.w;
+      cs[4] = hi.x; cs[5] = hi.y; cs[6] = hi.z; cs[7] = hi.w;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) cs[q] = (col + q < n) ? scale[col + q] : 0.f;
+    }
+  }
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int lr = ty + 16 * k;
     const int row = r0 + lr;
-    const int col = c0 + 4 * tx;
     if (row >= m || col >= n) continue;
-    float uu[4];
+    float uu[8];
     if (!tall) {
-      const uint2 pk = *reinterpret_cast<const uint2*>(u + static_cast<int64_t>(row) * ldu + col);
-      uu[0] = bf16_to_f32(pk.x & 0xffffu); uu[1] = bf16_to_f32(pk.x >> 16);
-      uu[2] = bf16_to_f32(pk.y & 0xffffu); uu[3] = bf16_to_f32(pk.y >> 16);
+      load8<true>(u, static_cast<int64_t>(row) * ldu + col, uu);
     } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) uu[q] = bf16_to_f32(tr[4 * tx + q][lr]);
+      for (int q = 0; q < 8; ++q) uu[q] = bf16_to_f32(tr[8 * tx + q][lr]);
     }
-    float s[4];
+    float s[8];
     if (dir == 0) {
       const float sr = scale[row];
-      s[0] = s[1] = s[2] = s[3] = sr;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) s[q] = sr;
     } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s[q] = (col + q < n) ? scale[col + q] : 0.f;
+      for (int q = 0; q < 8; ++q) s[q] = cs[q];
     }
     const int64_t off = static_cast<int64_t>(row) * n + col;
-    if (kParamBf16) {
-      uint16_t* wp = static_cast<uint16_t*>(a.w[mi]);
-      if (vec) {
-        uint2 pk = *reinterpret_cast<const uint2*>(wp + off);
-        float w[4] = {bf16_to_f32(pk.x & 0xffffu), bf16_to_f32(pk.x >> 16), bf16_to_f32(pk.y & 0xffffu),
-                      bf16_to_f32(pk.y >> 16)};
-        uint16_t h[4];
+    if (vec) {
+      float w[8];
+      load8<kParamBf16>(a.w[mi], off, w);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) h[q] = f32_to_bf16(fmaf(decay, w[q], -step * (uu[q] * s[q])));
-        pk.x = h[0] | (static_cast<uint32_t>(h[1]) << 16);
-        pk.y = h[2] | (static_cast<uint32_t>(h[3]) << 16);
-        *reinterpret_cast<uint2*>(wp + off) = pk;
+      for (int q = 0; q < 8; ++q) w[q] = fmaf(decay, w[q], -step * (uu[q] * s[q]));
+      if (kParamBf16) {
+        uint16_t h[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) h[q] = f32_to_bf16(w[q]);
+        *reinterpret_cast<uint4*>(static_cast<uint16_t*>(a.w[mi]) + off) = pack_bf16x8(h);
       } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (col + q < n) wp[off + q] = f32_to_bf16(fmaf(decay, bf16_to_f32(wp[off + q]), -step * (uu[q] * s[q])));
+        float* wp = static_cast<float*>(a.w[mi]);
+        *reinterpret_cast<float4*>(wp + off) = make_float4(w[0], w[1], w[2], w[3]);
+        *reinterpret_cast<float4*>(wp + off + 4) = make_float4(w[4], w[5], w[6], w[7]);
       }
     } else {
-      float* wp = static_cast<float*>(a.w[mi]);
-      if (vec) {
-        float4 wv = *reinterpret_cast<const float4*>(wp + off);
-        wv.x = fmaf(decay, wv.x, -step * (uu[0] * s[0]));
-        wv.y = fmaf(decay, wv.y, -step * (uu[1] * s[1]));
-        wv.z = fmaf(decay, wv.z, -step * (uu[2] * s[2]));
-        wv.w = fmaf(decay, wv.w, -step * (uu[3] * s[3]));
-        *reinterpret_cast<float4*>(wp + off) = wv;
-      } else {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (col + q < n) wp[off + q] = fmaf(decay, wp[off + q], -step * (uu[q] * s[q]));
+      for (int q = 0; q < 8; ++q) {
+        if (col + q >= n) break;
+        if (kParamBf16) {
+          uint16_t* wp = static_cast<uint16_t*>(a.w[mi]);
+          wp[off + q] = f32_to_bf16(fmaf(decay, bf16_to_f32(wp[off + q]), -step * (uu[q] * s[q])));
+        } else {
+          float* wp = static_cast<float*>(a.w[mi]);
+          wp[off + q] = fmaf(decay, wp[off + q], -step * (uu[q] * s[q]));
+        }
       }
     }
   }

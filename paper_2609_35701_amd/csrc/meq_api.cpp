@@ -34,8 +34,8 @@ struct MatInfo {
   bool tall;
   int dtype;  // param dtype == grad dtype
   int group, gidx;
-  int tiles_pad_r, tiles_pad_c;  // 64x64 tiles over the padded matrix in its own orientation
-  int tiles_upd_r, tiles_upd_c;  // 64x64 tiles over the real matrix
+  int tiles_pad_r, tiles_pad_c;  // kEwRows x kEwCols tiles over the padded matrix in its own orientation
+  int tiles_upd_r, tiles_upd_c;  // kEwRows x kEwCols tiles over the real matrix
   size_t off_part, off_rrms, off_crms, off_scale;
   // aux and vector plans
   int row_blocks;
@@ -189,10 +189,10 @@ meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hpa
     mi.L = round_up(mi.l, kTile);
     mi.dtype = mats[i].param_dtype;
     const int64_t pad_r = mi.tall ? mi.L : mi.S, pad_c = mi.tall ? mi.S : mi.L;
-    mi.tiles_pad_r = static_cast<int>(pad_r / kEwTile);
-    mi.tiles_pad_c = static_cast<int>(pad_c / kEwTile);
-    mi.tiles_upd_r = static_cast<int>((mi.m + kEwTile - 1) / kEwTile);
-    mi.tiles_upd_c = static_cast<int>((mi.n + kEwTile - 1) / kEwTile);
+    mi.tiles_pad_r = static_cast<int>(pad_r / kEwRows);
+    mi.tiles_pad_c = static_cast<int>(pad_c / kEwCols);
+    mi.tiles_upd_r = static_cast<int>((mi.m + kEwRows - 1) / kEwRows);
+    mi.tiles_upd_c = static_cast<int>((mi.n + kEwCols - 1) / kEwCols);
     auto key = std::make_pair(mi.s, mi.l);
     auto it = group_of.find(key);
     if (it == group_of.end()) {
@@ -524,6 +524,7 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
       a.ldx[k] = g.L;
       a.g[k] = grads[ch[k]];
       a.b[k] = momenta[ch[k]];
+      a.vec[k] = (mi.n % 8 == 0) && aligned(a.b[k], 16) && aligned(a.g[k], 16);
       a.x[k] = reinterpret_cast<uint16_t*>(ws + g.off_xa) + mi.gidx * g.stride_x;
       a.part[k] = reinterpret_cast<float*>(ws + mi.off_part);
     }
@@ -680,6 +681,7 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
       a.tall[k] = mi.tall;
       a.ldu[k] = g.L;
       a.w[k] = params[ch[k]];
+      a.vec[k] = (mi.n % 8 == 0) && aligned(a.w[k], 16);
       const size_t uoff = (hp.ns_steps % 2 == 1) ? g.off_xb : g.off_xa;
       a.u[k] = reinterpret_cast<const uint16_t*>(ws + uoff) + mi.gidx * g.stride_x;
       a.scale[k] = reinterpret_cast<const float*>(ws + mi.off_scale);

@@ -10,8 +10,10 @@ namespace meq {
 // so the GEMM kernels never need bounds checks.  Zero padding is exact for the
 // iteration: zero rows/columns of X stay zero through X X^T, A A and P X.
 constexpr int kTile = 256;
-// Element-wise kernels work on 64 x 64 tiles of the matrix's own orientation.
-constexpr int kEwTile = 64;
+// The momentum and write-back kernels work on kEwRows x kEwCols tiles of the matrix's own
+// orientation; each thread owns 8 consecutive columns of 4 rows.
+constexpr int kEwRows = 64;
+constexpr int kEwCols = 128;
 // Matrices per launch of the multi-matrix element-wise kernels (pointers travel as kernel arguments).
 constexpr int kMaxChunk = 32;
 
@@ -32,10 +34,11 @@ struct MomentumArgs {
   int count;
   int nesterov;
   float mu;
-  int tile_start[kMaxChunk + 1];  // prefix sum of 64x64 tiles over the padded matrix
+  int tile_start[kMaxChunk + 1];  // prefix sum of tiles over the padded matrix
   int m[kMaxChunk], n[kMaxChunk];
-  int tiles_c[kMaxChunk];         // 64-wide tile columns of the padded matrix (own orientation)
+  int tiles_c[kMaxChunk];         // tile columns of the padded matrix (own orientation)
   int tall[kMaxChunk];
+  int vec[kMaxChunk];             // n % 8 == 0 and aligned pointers: 8-element vector access
   int64_t ldx[kMaxChunk];         // leading dimension of the wide bf16 buffer (padded long side)
   const void* g[kMaxChunk];
   float* b[kMaxChunk];
@@ -116,6 +119,7 @@ struct UpdateArgs {
   float step;   // rho * lr
   int tile_start[kMaxChunk + 1];
   int m[kMaxChunk], n[kMaxChunk], tiles_c[kMaxChunk], tall[kMaxChunk];
+  int vec[kMaxChunk];  // n % 8 == 0 and an aligned parameter pointer
   int64_t ldu[kMaxChunk];
   void* w[kMaxChunk];
   const uint16_t* u[kMaxChunk];
