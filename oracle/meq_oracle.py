@@ -276,3 +276,18 @@ def moonlight_step(w: np.ndarray, g: np.ndarray, b_prev: np.ndarray, hp: HParams
     ut = math.sqrt(max(m, n)) * u
     w_new = write_back(w, ut, lr, hp.rho, hp.weight_decay)
     return {"W": w_new, "B": b, "V": v, "normsq": frobenius(v) ** 2, "U": u, "Ut": ut}
+
+
+# ------------------------------------------- NS trajectories (Section "Imbalance patterns")
+def ns_cv_trace(v: np.ndarray, hp: HParams, kmax: int, wide: bool = False):
+    """Row and column CVs of X_k for k = 0 .. kmax, where X_0 = V / ||V||_F and X_k follows
+    eq. "ns"; the replay behind the paper's figure of CV trajectories during the NS iterations.
+    Returns two lists of kmax + 1 values (gamma_r, gamma_c)."""
+    gr, gc = [], []
+    for k in range(kmax + 1):
+        x = (np.asarray(v, np.float64) / frobenius(v) if k == 0 else
+             newton_schulz(v, hp.ns_a, hp.ns_b, hp.ns_c, k, wide=wide))
+        r, c = row_col_rms(x)
+        gr.append(coeff_of_variation(r, hp.delta))
+        gc.append(coeff_of_variation(c, hp.delta))
+    return gr, gc

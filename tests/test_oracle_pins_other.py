@@ -179,3 +179,38 @@ def test_moonlight_update_rms_matches_rho_for_orthogonal_u():
         out = oracle.moonlight_step(w, g, np.zeros(shape), hp, 0.5)
         upd_rms = math.sqrt(float(np.mean(out["W"] ** 2)))
         assert abs(upd_rms - 0.2 * 0.5) < 1e-9
+
+
+# ------------------------------------------------------------- NS CV trajectories
+def test_ns_cv_trace_start_and_end_points():
+    hp = HParams()
+    v = rng(30).standard_normal((24, 40)) * np.exp(rng(31).standard_normal((24, 1)))
+    gr, gc = oracle.ns_cv_trace(v, hp, 6)
+    assert len(gr) == len(gc) == 7
+    # k = 0 is the input itself (CVs are scale free): brute force
+    rr, cc = rms_rows_cols_loops(v)
+    for got, vals in ((gr[0], rr), (gc[0], cc)):
+        mean = sum(vals) / len(vals)
+        want = math.sqrt(sum((t - mean) ** 2 for t in vals) / len(vals)) / mean
+        assert abs(got - want) < 1e-12
+    # k = K is what the update equilibrates
+    hp5 = HParams(ns_steps=5)
+    out = oracle.meq_step(np.zeros_like(v), v, np.zeros_like(v), hp5, 0.0)
+    assert abs(gr[5] - out["gamma_r"]) < 1e-12 and abs(gc[5] - out["gamma_c"]) < 1e-12
+
+
+@pytest.mark.parametrize("shape,zero_side", [((20, 50), "rows"), ((50, 20), "cols"), ((30, 30), "both")])
+def test_ns_cv_trace_orthogonality_constraints(shape, zero_side):
+    # exact orthogonalization equalizes the short side's magnitudes (Y Y^T = I for m < n,
+    # Y^T Y = I for m > n, both when square); a convergent quintic reaches it
+    hp = HParams(ns_a=15 / 8, ns_b=-10 / 8, ns_c=3 / 8)
+    v = rng(32).standard_normal(shape) * np.exp(rng(33).standard_normal((shape[0], 1)))
+    gr, gc = oracle.ns_cv_trace(v, hp, 60)
+    if zero_side in ("rows", "both"):
+        assert gr[-1] < 1e-9
+    if zero_side in ("cols", "both"):
+        assert gc[-1] < 1e-9
+    if zero_side == "rows":
+        assert gc[-1] > 0.05
+    if zero_side == "cols":
+        assert gr[-1] > 0.05
