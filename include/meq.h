@@ -30,7 +30,7 @@
  *   - Functions that return meq_status validate every argument before any
  *     device work; on an argument error nothing is enqueued and no caller
  *     memory is modified.  HIP failures are reported as MEQ_ERR_HIP.
- *   - No entry point blocks the host except meq_get_stats and
+ *   - No entry point blocks the host except meq_get_stats, meq_ns_cv_trace and
  *     meq_get_timing, which synchronize with the given stream.
  *   - A plan is not reentrant: do not run two meq_step calls of one plan (or
  *     two plans sharing one workspace) concurrently on different streams.
@@ -167,6 +167,20 @@ meq_status meq_step(meq_plan* plan, void* const* params, const void* const* grad
  */
 meq_status meq_get_stats(const meq_plan* plan, const void* workspace, double* gamma_r, double* gamma_c,
                          int32_t* dir, hipStream_t stream);
+
+/*
+ * Diagnostics: the row and column CVs of X_k for k = 0 .. kmax (eq. "cv" of the row/column
+ * RMS of eq. "row-col-rms"), where X_0 = V / ||V||_F is formed from inputs[i] (device
+ * pointer, rows x cols of the matrix's param dtype, read only) and X_k follows eq. "ns" with
+ * the plan's coefficients; the replay behind the paper's CV trajectories of the NS
+ * iterations (Section "Imbalance patterns").  Runs on the plan's own kernels, uses the
+ * workspace (its statistics are overwritten) and touches no parameters or momenta.
+ * gamma_r and gamma_c are host arrays of count * (kmax + 1) doubles, matrix-major
+ * (entry i * (kmax + 1) + k).  A hidden plan only; 0 <= kmax <= 64.  Synchronizes with
+ * `stream` once per k.
+ */
+meq_status meq_ns_cv_trace(meq_plan* plan, const void* const* inputs, int32_t kmax, void* workspace,
+                           size_t workspace_bytes, double* gamma_r, double* gamma_c, hipStream_t stream);
 
 /* Release a plan (null is a no-op).  Pending timing events are destroyed. */
 void meq_destroy(meq_plan* plan);

@@ -78,6 +78,7 @@ __device__ __forceinline__ uint4 pack_bf16x8(const uint16_t (&h)[8]) {
 // --------------------------------------------------------------------------------
 // Momentum B <- mu B + G, V = B (or G + mu B), per-tile sum of V^2, bf16 V written
 // into the zero-padded wide buffer (transposed through LDS for tall matrices).
+// Without a momentum buffer (b == nullptr) V is the input G itself.
 // One block = one 64 x 128 tile of the padded matrix in its own orientation;
 // thread (ty, tx) owns rows ty + 16 k (k < 4) and columns 8 tx .. 8 tx + 7.
 template <bool kGradBf16>
@@ -104,7 +105,17 @@ __global__ __launch_bounds__(256) void k_momentum(MomentumArgs a) {
     float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (row < m && col < n) {
       const int64_t off = static_cast<int64_t>(row) * n + col;
-      if (vec) {
+      if (!bp) {
+        if (vec) {
+          load8<kGradBf16>(a.g[mi], off, v);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            if (col + q < n)
+              v[q] = kGradBf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.g[mi])[off + q])
+                               : static_cast<const float*>(a.g[mi])[off + q];
+        }
+      } else if (vec) {
         float g[8], b[8];
         load8<kGradBf16>(a.g[mi], off, g);
         load8<false>(bp, off, b);

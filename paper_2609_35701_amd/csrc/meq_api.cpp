@@ -471,26 +471,11 @@ meq_status step_vec(meq_plan* p, void* const* params, const void* const* grads, 
 
 }  // namespace
 
-MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* const* grads, float* const* momenta,
-                               float lr, void* workspace, size_t workspace_bytes, hipStream_t st) {
-  if (!p) return MEQ_ERR_INVALID_ARG;
+namespace {
+
+// Element-wise kernels run over chunks of matrices sharing a dtype.
+std::vector<std::vector<int>> dtype_chunks(const meq_plan* p) {
   const int count = static_cast<int>(p->mats.size());
-  if (!std::isfinite(lr) || lr < 0.f) return MEQ_ERR_INVALID_ARG;
-  if (count == 0) return MEQ_OK;
-  if (!params || !grads || !momenta) return MEQ_ERR_INVALID_ARG;
-  for (int i = 0; i < count; ++i)
-    if (!params[i] || !grads[i] || !momenta[i]) return MEQ_ERR_INVALID_ARG;
-  if (!workspace || workspace_bytes < p->ws_bytes || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
-    return MEQ_ERR_WORKSPACE;
-
-  char* ws = static_cast<char*>(workspace);
-  if (p->kind == MEQ_PARAM_AUX) return step_aux(p, params, grads, momenta, lr, ws, st);
-  if (p->kind == MEQ_PARAM_VECTOR) return step_vec(p, params, grads, momenta, lr, ws, st);
-  MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
-  const meq_hparams& hp = p->hp;
-  const bool moonlight = hp.update_rule == MEQ_RULE_MOONLIGHT;
-
-  // Element-wise kernels run over chunks of matrices sharing a dtype.
   std::vector<std::vector<int>> chunks;
   for (int dt = 0; dt < 2; ++dt) {
     std::vector<int> cur;
@@ -504,7 +489,16 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     }
     if (!cur.empty()) chunks.push_back(cur);
   }
+  return chunks;
+}
 
+// Steps a1-a2: momentum (or, with momenta == nullptr, V = the given inputs), bf16 V in wide
+// orientation, ||V||_F^2 and its reciprocals.
+meq_status enqueue_prescale(meq_plan* p, char* ws, const void* const* grads, float* const* momenta, hipStream_t st) {
+  const meq_hparams& hp = p->hp;
+  const int count = static_cast<int>(p->mats.size());
+  MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
+  const auto chunks = dtype_chunks(p);
   // 1. momentum + bf16 V (wide, zero-padded) + per-tile ||V||^2 partials
   for (const auto& ch : chunks) {
     MomentumArgs a{};
@@ -523,7 +517,7 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
       a.tall[k] = mi.tall;
       a.ldx[k] = g.L;
       a.g[k] = grads[ch[k]];
-      a.b[k] = momenta[ch[k]];
+      a.b[k] = momenta ? momenta[ch[k]] : nullptr;  // none: V is the input itself
       a.vec[k] = (mi.n % 8 == 0) && aligned(a.b[k], 16) && aligned(a.g[k], 16);
       a.x[k] = reinterpret_cast<uint16_t*>(ws + g.off_xa) + mi.gidx * g.stride_x;
       a.part[k] = reinterpret_cast<float*>(ws + mi.off_part);
@@ -545,12 +539,17 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     }
     MEQ_TRY(timed_launch(p, MEQ_K_NORM, st, [&] { return launch_norm(a, st); }));
   }
-  // 3. Newton-Schulz: per step one launch per product over all shape groups (chunks of
-  //    kMaxGemmGroups), longest K first so the long tiles start first.  Ping-pong between
-  //    buffers a (holding X_0) and b.
+  return MEQ_OK;
+}
+
+// Step a3, iteration k of eq. "ns": per product one launch over all shape groups (chunks of
+// kMaxGemmGroups), longest K first so the long tiles start first.  Ping-pong between buffers
+// a (holding X_0) and b: iteration k reads a when k is even.
+meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, hipStream_t st) {
+  const meq_hparams& hp = p->hp;
   std::vector<int> order(p->groups.size());
   for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int>(i);
-  for (int k = 0; k < hp.ns_steps; ++k) {
+  {
     const bool from_a = (k % 2) == 0;
     for (int kind = 0; kind < 3; ++kind) {
       // kind 0: Gram (K = L), 1: polynomial (K = S), 2: apply (K = S)
@@ -612,6 +611,15 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
       }
     }
   }
+  return MEQ_OK;
+}
+
+// Steps a4-a5 on the Newton-Schulz output in buffer b (u_in_b) or a: row/column RMS, CVs,
+// direction and scale vectors; with the Moonlight rule only the uniform scale.
+meq_status enqueue_stats(meq_plan* p, char* ws, bool u_in_b, bool moonlight, hipStream_t st) {
+  const meq_hparams& hp = p->hp;
+  const int count = static_cast<int>(p->mats.size());
+  MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
   // 4. row / column sums of squares of U, per shape group (MeqMuon only)
   for (size_t gi = 0; gi < p->groups.size() && !moonlight; ++gi) {
     const GroupInfo& g = p->groups[gi];
@@ -620,7 +628,7 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     uint16_t* xa = reinterpret_cast<uint16_t*>(ws + g.off_xa);
     uint16_t* xb = reinterpret_cast<uint16_t*>(ws + g.off_xb);
     RowColArgs rc{};
-    rc.u = (hp.ns_steps % 2 == 1) ? xb : xa;
+    rc.u = u_in_b ? xb : xa;
     rc.stride_u = g.stride_x;
     rc.S = static_cast<int>(g.S);
     rc.L = static_cast<int>(g.L);
@@ -661,6 +669,14 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
       MEQ_TRY(timed_launch(p, MEQ_K_SELECT, st, [&] { return launch_select(a, st); }));
     }
   }
+  return MEQ_OK;
+}
+
+// Step a6: decoupled weight decay and the normalized update.
+meq_status enqueue_update(meq_plan* p, char* ws, void* const* params, float lr, hipStream_t st) {
+  const meq_hparams& hp = p->hp;
+  MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
+  const auto chunks = dtype_chunks(p);
   // 6. write-back
   const float decay = static_cast<float>(1.0 - static_cast<double>(lr) * hp.weight_decay);
   const float stepc = static_cast<float>(static_cast<double>(hp.rho) * lr);
@@ -690,6 +706,60 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     a.tile_start[a.count] = tiles;
     const int pbf = p->mats[ch[0]].dtype == MEQ_BF16;
     MEQ_TRY(timed_launch(p, MEQ_K_UPDATE, st, [&] { return launch_update(a, pbf, tiles, st); }));
+  }
+  return MEQ_OK;
+}
+
+}  // namespace
+
+MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* const* grads, float* const* momenta,
+                               float lr, void* workspace, size_t workspace_bytes, hipStream_t st) {
+  if (!p) return MEQ_ERR_INVALID_ARG;
+  const int count = static_cast<int>(p->mats.size());
+  if (!std::isfinite(lr) || lr < 0.f) return MEQ_ERR_INVALID_ARG;
+  if (count == 0) return MEQ_OK;
+  if (!params || !grads || !momenta) return MEQ_ERR_INVALID_ARG;
+  for (int i = 0; i < count; ++i)
+    if (!params[i] || !grads[i] || !momenta[i]) return MEQ_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < p->ws_bytes || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return MEQ_ERR_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  if (p->kind == MEQ_PARAM_AUX) return step_aux(p, params, grads, momenta, lr, ws, st);
+  if (p->kind == MEQ_PARAM_VECTOR) return step_vec(p, params, grads, momenta, lr, ws, st);
+  const meq_hparams& hp = p->hp;
+  MEQ_TRY(enqueue_prescale(p, ws, grads, momenta, st));
+  for (int k = 0; k < hp.ns_steps; ++k) MEQ_TRY(enqueue_ns_iteration(p, ws, k, st));
+  MEQ_TRY(enqueue_stats(p, ws, hp.ns_steps % 2 == 1, hp.update_rule == MEQ_RULE_MOONLIGHT, st));
+  MEQ_TRY(enqueue_update(p, ws, params, lr, st));
+  return MEQ_OK;
+}
+
+MEQ_EXPORT meq_status meq_ns_cv_trace(meq_plan* p, const void* const* inputs, int32_t kmax, void* workspace,
+                                      size_t workspace_bytes, double* gamma_r, double* gamma_c, hipStream_t st) {
+  if (!p || p->kind != MEQ_PARAM_HIDDEN || kmax < 0 || kmax > 64) return MEQ_ERR_INVALID_ARG;
+  const int count = static_cast<int>(p->mats.size());
+  if (count == 0) return MEQ_OK;
+  if (!inputs || !gamma_r || !gamma_c) return MEQ_ERR_INVALID_ARG;
+  for (int i = 0; i < count; ++i)
+    if (!inputs[i]) return MEQ_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < p->ws_bytes || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return MEQ_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  std::vector<MatScalars> host(count);
+  const char* src = ws + p->off_scal;
+  MEQ_TRY(enqueue_prescale(p, ws, inputs, nullptr, st));
+  for (int k = 0; k <= kmax; ++k) {
+    if (k > 0) MEQ_TRY(enqueue_ns_iteration(p, ws, k - 1, st));
+    // X_0 (unscaled V: CVs are scale free) sits in buffer a; iteration k - 1 writes b for odd k
+    MEQ_TRY(enqueue_stats(p, ws, k % 2 == 1, false, st));
+    if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
+      return MEQ_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;
+    for (int i = 0; i < count; ++i) {
+      gamma_r[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_r;
+      gamma_c[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_c;
+    }
   }
   return MEQ_OK;
 }

@@ -25,7 +25,7 @@ KERNEL_NAMES = ("momentum", "norm", "gram", "poly", "apply", "rowcol", "select",
                 "aux_rows", "aux_cols", "aux_update", "vector")
 
 EXPORTED = ("meq_default_hparams", "meq_init", "meq_init_kind", "meq_workspace_bytes", "meq_step",
-            "meq_get_stats", "meq_destroy", "meq_status_string", "meq_plan_num_groups", "meq_plan_group",
+            "meq_get_stats", "meq_ns_cv_trace", "meq_destroy", "meq_status_string", "meq_plan_num_groups", "meq_plan_group",
             "meq_debug_region", "meq_set_timing", "meq_get_timing")
 
 
@@ -76,6 +76,9 @@ def lib() -> ctypes.CDLL:
     L.meq_get_stats.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                 ctypes.POINTER(c_i32), vp]
     L.meq_get_stats.restype = c_i32
+    L.meq_ns_cv_trace.argtypes = [vp, ctypes.POINTER(vp), c_i32, vp, c_sz, ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(ctypes.c_double), vp]
+    L.meq_ns_cv_trace.restype = c_i32
     L.meq_destroy.argtypes = [vp]
     L.meq_destroy.restype = None
     L.meq_status_string.argtypes = [c_i32]
@@ -196,6 +199,19 @@ class Plan:
                "meq_get_stats")
         return list(gr)[:n], list(gc)[:n], list(d)[:n]
 
+    def ns_cv_trace_ptr(self, inputs: Sequence[int], kmax: int, workspace: int, workspace_bytes: int,
+                        stream: int = 0):
+        """Row and column CVs of X_0 .. X_kmax per matrix (``meq_ns_cv_trace``)."""
+        n = self.count
+        X = (ctypes.c_void_p * max(n, 1))(*inputs)
+        gr = (ctypes.c_double * max(n * (kmax + 1), 1))()
+        gc = (ctypes.c_double * max(n * (kmax + 1), 1))()
+        _check(lib().meq_ns_cv_trace(self._h, X, int(kmax), ctypes.c_void_p(workspace),
+                                     ctypes.c_size_t(workspace_bytes), gr, gc, ctypes.c_void_p(stream)),
+               "meq_ns_cv_trace")
+        w = kmax + 1
+        return [list(gr)[i * w:(i + 1) * w] for i in range(n)], [list(gc)[i * w:(i + 1) * w] for i in range(n)]
+
     def set_timing(self, kinds: Iterable[int]) -> None:
         mask = 0
         for k in kinds:
@@ -276,6 +292,22 @@ class HiddenWeightUpdate(ParamUpdate):
     Moonlight-Muon rule with ``hparams.update_rule = RULE_MOONLIGHT``)."""
 
     kind = PARAM_HIDDEN
+
+
+def ns_cv_trace(upd: "HiddenWeightUpdate", inputs, kmax: int = 20, stream=None):
+    """CV trajectories of the Newton-Schulz iterates for ``inputs`` (one tensor per matrix of a
+    hidden update, shaped and typed like its parameters), using that update's plan and workspace."""
+    import torch
+
+    inputs = list(inputs)
+    if len(inputs) != len(upd.params):
+        raise ValueError("one input per parameter is required")
+    for x, p in zip(inputs, upd.params):
+        if x.shape != p.shape or x.dtype != p.dtype or not x.is_contiguous() or x.device != p.device:
+            raise ValueError("inputs must match their parameters in shape, dtype and device")
+    st = torch.cuda.current_stream(upd.params[0].device) if stream is None else stream
+    return upd.plan.ns_cv_trace_ptr([x.data_ptr() for x in inputs], kmax, upd.workspace.data_ptr(),
+                                    upd.workspace.numel(), st.cuda_stream)
 
 
 class AuxUpdate(ParamUpdate):

@@ -232,3 +232,25 @@ def test_kind_step_rejects_bad_arguments_before_any_device_work(kind):
     assert step(lr=float("inf")) == meq.MEQ_ERR_INVALID_ARG
     assert step(w=0) == meq.MEQ_ERR_WORKSPACE
     assert step(wb=ws - 1) == meq.MEQ_ERR_WORKSPACE
+
+
+def test_ns_cv_trace_rejects_bad_arguments_before_any_device_work():
+    L = meq.lib()
+    hid = meq.Plan([(4, 8), (16, 3)], "f32")
+    aux = meq.Plan([(4, 8)], "f32", kind=meq.PARAM_AUX)
+    X = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    Z = (ctypes.c_void_p * 2)(0x1000, 0)
+    gr = (ctypes.c_double * 64)()
+    gc = (ctypes.c_double * 64)()
+    ws = hid.workspace_bytes
+
+    def trace(plan=hid.handle, inputs=X, kmax=3, w=0x100000, wb=ws, r=gr, c=gc):
+        return L.meq_ns_cv_trace(plan, inputs, kmax, ctypes.c_void_p(w), wb, r, c, None)
+
+    assert trace(plan=aux.handle) == meq.MEQ_ERR_INVALID_ARG
+    assert trace(kmax=-1) == meq.MEQ_ERR_INVALID_ARG
+    assert trace(kmax=65) == meq.MEQ_ERR_INVALID_ARG
+    assert trace(inputs=Z) == meq.MEQ_ERR_INVALID_ARG
+    assert trace(r=None) == meq.MEQ_ERR_INVALID_ARG
+    assert trace(w=0) == meq.MEQ_ERR_WORKSPACE
+    assert trace(wb=ws - 1) == meq.MEQ_ERR_WORKSPACE

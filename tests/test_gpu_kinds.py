@@ -209,3 +209,42 @@ def test_moonlight_parity(shape, dtype):
         with pytest.raises(meq.MeqError):
             upd.stats()
         w, b = w_gpu, b_gpu
+
+
+# ------------------------------------------------ NS CV trajectories (diagnostics)
+def test_ns_cv_trace_matches_oracle():
+    # shapes of the paper's trajectory figure: square, wide and tall, with row imbalance.
+    # The bf16 iterates drift from the fp64 ones step by step (independent roundings), so the
+    # 3e-2 bound stated for five steps grows with the square root of the step count.
+    shapes = [(256, 256), (192, 576), (576, 192), (300, 100)]
+    hp = meq.default_hparams()
+    ohp = oracle_hp(hp)
+    wl = workloads.custom(shapes, "bf16", seed=41, sigma=1.5)
+    params = [to_dev(workloads.weight_init(wl, i), "bf16") for i in range(len(shapes))]
+    upd = meq.HiddenWeightUpdate(params, hp)
+    vs = [workloads.grad_at_step(wl, i, 0).astype(np.float64) for i in range(len(shapes))]
+    w_before = [p.clone() for p in params]
+    kmax = 20
+    log(f"ns cv trace {shapes} kmax={kmax}")
+    gr, gc = meq.ns_cv_trace(upd, [to_dev(v, "bf16") for v in vs], kmax)
+    worst = 0.0
+    for i, (shape, v) in enumerate(zip(shapes, vs)):
+        ogr, ogc = oracle.ns_cv_trace(v, ohp, kmax, wide=True)
+        for k in range(kmax + 1):
+            for got, want, side in ((gr[i][k], ogr[k], "row"), (gc[i][k], ogc[k], "col")):
+                err = abs(got - want)
+                tol = TOL_NS * max(want, 0.05) * math.sqrt(max(k, 5) / 5)
+                worst = max(worst, err / tol)
+                assert err <= tol, f"{shape} k={k} {side} CV {got} vs {want}"
+        # the short side's magnitudes flatten (rows for wide, columns for tall)
+        m, n = shape
+        if m < n:
+            assert gr[i][kmax] < 0.1 * gr[i][0]
+        if m > n:
+            assert gc[i][kmax] < 0.1 * gc[i][0]
+    log(f"ns cv trace worst CV error / bound {worst:.3g}")
+    # a trace touches neither the parameters nor the momenta
+    for p, w in zip(params, w_before):
+        assert torch.equal(p, w)
+    for b in upd.momenta:
+        assert not torch.any(b != 0)
