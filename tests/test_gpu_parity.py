@@ -190,17 +190,19 @@ def test_timing_events_report_every_kernel():
     assert run.upd.plan.get_timing(meq.K_APPLY) == (0.0, 0)
 
 
-def test_full_1b_launch_sampled_parity():
-    """The benchmark's launch configuration (all 112 matrices of the 1B shapes in one meq_step);
-    the first and last matrix of each shape group are seeded from the numpy generator and
-    checked against the oracle, the rest carry device-drawn inputs of the same recipe."""
-    wl = workloads.workload("llama-1b")
+@pytest.mark.parametrize("name", ["llama-350m", "llama-1b", "llama-7b-block-x4"])
+def test_full_launch_sampled_parity(name):
+    """A full-size workload in one meq_step (the 1B one is the benchmark's launch
+    configuration; the 7B block carries the extreme row/column imbalance); the first and last
+    matrix of each shape group are seeded from the numpy generator and checked against the
+    oracle, the rest carry device-drawn inputs of the same recipe."""
+    wl = workloads.workload(name)
     shapes = [(m.rows, m.cols) for m in wl.matrices]
     groups = {}
     for i, s in enumerate(shapes):
         groups.setdefault((min(s), max(s)), []).append(i)
     sample = sorted({g[0] for g in groups.values()} | {g[-1] for g in groups.values()})
-    log(f"[case] llama-1b full launch, sampled matrices {sample}")
+    log(f"[case] {name} full launch, sampled matrices {sample}")
     params, grads, _ = workloads.device_inputs(wl, DEV)
     w_np, g_np = {}, {}
     for i in sample:
