@@ -146,11 +146,14 @@ def ns_flops(s: int, l: int, steps: int):
     return sym, apply, dense
 
 
-def stage_bytes(elems: int, param_bytes: int):
+def stage_bytes(elems: int, param_bytes: int, rowcol_pass: bool):
     """Algorithmic HBM bytes per element of the byte stages: momentum (G, B read+write, bf16 V),
-    row/column sums (U), write-back (U, W read+write)."""
-    return {"momentum": elems * (param_bytes + 4 + 4 + 2), "rowcol": elems * 2,
-            "update": elems * (2 + 2 * param_bytes)}
+    row/column sums (U, only when they run as a pass of their own rather than in the last
+    apply product's epilogue), write-back (U, W read+write)."""
+    out = {"momentum": elems * (param_bytes + 4 + 4 + 2), "update": elems * (2 + 2 * param_bytes)}
+    if rowcol_pass:
+        out["rowcol"] = elems * 2
+    return out
 
 
 def time_steps(upd, grads, lr: float, steps: int, warmup: int, kinds) -> dict:
@@ -348,7 +351,7 @@ def main() -> int:
         a, b, c = ns_flops(s, l, hp.ns_steps)
         sym, apply, dense = sym + a, apply + b, dense + c
     pbytes = 2 if wl.param_dtype == "bf16" else 4
-    sb = stage_bytes(wl.elements, pbytes)
+    sb = stage_bytes(wl.elements, pbytes, kern["rowcol"]["launches_per_step"] > 0)
     ns_ms = sum(kern[k]["ms_per_step"] for k in ("gram", "poly", "apply"))
     ap_ms = kern["apply"]["ms_per_step"]
     apply_tflops = apply / (ap_ms * 1e-3) / 1e12
@@ -362,11 +365,12 @@ def main() -> int:
         "ns_frac_of_peak_sym": sym / (ns_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
         "ns_tflops_dense": dense / (ns_ms * 1e-3) / 1e12,
         "momentum_gbs": sb["momentum"] / (kern["momentum"]["ms_per_step"] * 1e-3) / 1e9,
-        "rowcol_gbs": sb["rowcol"] / (kern["rowcol"]["ms_per_step"] * 1e-3) / 1e9,
         "update_gbs": sb["update"] / (kern["update"]["ms_per_step"] * 1e-3) / 1e9,
-        "byte_stages_gbs": sum(sb.values()) / (sum(kern[k]["ms_per_step"] for k in ("momentum", "rowcol", "update"))
-                                               * 1e-3) / 1e9,
+        "byte_stages_ms": sum(kern[k]["ms_per_step"] for k in sb),
+        "byte_stages_gbs": sum(sb.values()) / (sum(kern[k]["ms_per_step"] for k in sb) * 1e-3) / 1e9,
     }
+    if "rowcol" in sb:
+        stages["rowcol_gbs"] = sb["rowcol"] / (kern["rowcol"]["ms_per_step"] * 1e-3) / 1e9
     extras = None
     if not args.no_extras and wl.name == "llama-1b":
         print("# bench: other parameter kinds and the Moonlight-Muon rule", file=sys.stderr, flush=True)

@@ -113,6 +113,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   __shared__ __attribute__((aligned(1024))) uint8_t st1_[kStageBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t st2_[kStageBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t st3_[kStageBytes];
+  __shared__ float colsum_[kNN ? 4 : 1][256];  // apply: per-wave column partials of the fused sums
   lds_u8* const st0 = (lds_u8*)st0_;
   lds_u8* const st1 = (lds_u8*)st1_;
   lds_u8* const st2 = (lds_u8*)st2_;
@@ -383,6 +384,45 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
     }
   __syncthreads();
+
+  if (kNN && g.rpart) {
+    // Row and column sums of squares of this bf16 output tile, read back from its staged
+    // copy in a fixed order.  Row t: its 32 16-byte chunks, thread t starting at chunk t % 32 so
+    // the 16 lanes of an LDS pass hit 16 different bank groups.  Columns: wave w sums its own
+    // stage (rows 64 w .. 64 w + 63), 4 columns per lane, and the four waves meet in LDS.
+    const lds_u8* srow = stage_of(t >> 6);
+    float rsum = 0.f;
+#pragma unroll 8
+    for (int p = 0; p < 32; ++p) {
+      const int slot = (p + t) & 31;
+      const u32x4 v = *reinterpret_cast<const lds_u32x4*>(srow + (t & 63) * 512 + 16 * slot);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = bf16_to_f32(v[e] & 0xffffu), hi = bf16_to_f32(v[e] >> 16);
+        rsum = fmaf(lo, lo, rsum);
+        rsum = fmaf(hi, hi, rsum);
+      }
+    }
+    const int c4 = 4 * lane;  // columns c4 .. c4 + 3
+    const lds_u8* sw = stage_of(wave);
+    float cs[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 16
+    for (int rr = 0; rr < 64; ++rr) {
+      const u32x2 v = *reinterpret_cast<const lds_u32x2*>(sw + stage_byte(64 * wave + rr, c4));
+      const float x0 = bf16_to_f32(v.x & 0xffffu), x1 = bf16_to_f32(v.x >> 16);
+      const float x2 = bf16_to_f32(v.y & 0xffffu), x3 = bf16_to_f32(v.y >> 16);
+      cs[0] = fmaf(x0, x0, cs[0]);
+      cs[1] = fmaf(x1, x1, cs[1]);
+      cs[2] = fmaf(x2, x2, cs[2]);
+      cs[3] = fmaf(x3, x3, cs[3]);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) colsum_[wave][c4 + q] = cs[q];
+    __syncthreads();
+    const float csum = (colsum_[0][t] + colsum_[1][t]) + (colsum_[2][t] + colsum_[3][t]);
+    g.rpart[mat * g.stride_rpart + static_cast<int64_t>(tj) * (g.tiles_m * 256) + rowA0 + t] = rsum;
+    g.cpart[mat * g.stride_cpart + static_cast<int64_t>(ti) * g.ldc + rowB0 + t] = csum;
+  }
 
   // whole-row stores of OUT: each wave instruction writes 2 full rows
   uint16_t* __restrict__ C = g.c + mat * g.stride_c;

@@ -544,8 +544,9 @@ meq_status enqueue_prescale(meq_plan* p, char* ws, const void* const* grads, flo
 
 // Step a3, iteration k of eq. "ns": per product one launch over all shape groups (chunks of
 // kMaxGemmGroups), longest K first so the long tiles start first.  Ping-pong between buffers
-// a (holding X_0) and b: iteration k reads a when k is even.
-meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, hipStream_t st) {
+// a (holding X_0) and b: iteration k reads a when k is even.  With `rowcol` the apply
+// product also writes the row/column sums of squares of its output (step a4's partials).
+meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, bool rowcol, hipStream_t st) {
   const meq_hparams& hp = p->hp;
   std::vector<int> order(p->groups.size());
   for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int>(i);
@@ -600,6 +601,12 @@ meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, hipStream_t st) {
             gg.e = nullptr; gg.lde = 0; gg.stride_e = 0;
             gg.K = static_cast<int>(g.S);
             gg.tiles_m = tm; gg.tiles_n = tn; gg.tiles_per_mat = tm * tn;
+            if (rowcol) {
+              gg.rpart = reinterpret_cast<float*>(ws + g.off_rpart);
+              gg.cpart = reinterpret_cast<float*>(ws + g.off_cpart);
+              gg.stride_rpart = g.stride_rpart;
+              gg.stride_cpart = g.stride_cpart;
+            }
           }
           gg.tiles = gg.tiles_per_mat * batch;
           ga.tile_start[q] = start;
@@ -615,13 +622,14 @@ meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, hipStream_t st) {
 }
 
 // Steps a4-a5 on the Newton-Schulz output in buffer b (u_in_b) or a: row/column RMS, CVs,
-// direction and scale vectors; with the Moonlight rule only the uniform scale.
-meq_status enqueue_stats(meq_plan* p, char* ws, bool u_in_b, bool moonlight, hipStream_t st) {
+// direction and scale vectors; with the Moonlight rule only the uniform scale.  With
+// `sums_done` the row/column sums of squares were already written by the last apply product.
+meq_status enqueue_stats(meq_plan* p, char* ws, bool u_in_b, bool moonlight, bool sums_done, hipStream_t st) {
   const meq_hparams& hp = p->hp;
   const int count = static_cast<int>(p->mats.size());
   MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
   // 4. row / column sums of squares of U, per shape group (MeqMuon only)
-  for (size_t gi = 0; gi < p->groups.size() && !moonlight; ++gi) {
+  for (size_t gi = 0; gi < p->groups.size() && !moonlight && !sums_done; ++gi) {
     const GroupInfo& g = p->groups[gi];
     const int batch = static_cast<int>(g.mats.size());
     const int tm = static_cast<int>(g.S / kTile), tn = static_cast<int>(g.L / kTile);
@@ -728,9 +736,11 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
   if (p->kind == MEQ_PARAM_AUX) return step_aux(p, params, grads, momenta, lr, ws, st);
   if (p->kind == MEQ_PARAM_VECTOR) return step_vec(p, params, grads, momenta, lr, ws, st);
   const meq_hparams& hp = p->hp;
+  const bool moonlight = hp.update_rule == MEQ_RULE_MOONLIGHT;
   MEQ_TRY(enqueue_prescale(p, ws, grads, momenta, st));
-  for (int k = 0; k < hp.ns_steps; ++k) MEQ_TRY(enqueue_ns_iteration(p, ws, k, st));
-  MEQ_TRY(enqueue_stats(p, ws, hp.ns_steps % 2 == 1, hp.update_rule == MEQ_RULE_MOONLIGHT, st));
+  for (int k = 0; k < hp.ns_steps; ++k)
+    MEQ_TRY(enqueue_ns_iteration(p, ws, k, !moonlight && k == hp.ns_steps - 1, st));
+  MEQ_TRY(enqueue_stats(p, ws, hp.ns_steps % 2 == 1, moonlight, !moonlight, st));
   MEQ_TRY(enqueue_update(p, ws, params, lr, st));
   return MEQ_OK;
 }
@@ -750,9 +760,9 @@ MEQ_EXPORT meq_status meq_ns_cv_trace(meq_plan* p, const void* const* inputs, in
   const char* src = ws + p->off_scal;
   MEQ_TRY(enqueue_prescale(p, ws, inputs, nullptr, st));
   for (int k = 0; k <= kmax; ++k) {
-    if (k > 0) MEQ_TRY(enqueue_ns_iteration(p, ws, k - 1, st));
+    if (k > 0) MEQ_TRY(enqueue_ns_iteration(p, ws, k - 1, false, st));
     // X_0 (unscaled V: CVs are scale free) sits in buffer a; iteration k - 1 writes b for odd k
-    MEQ_TRY(enqueue_stats(p, ws, k % 2 == 1, false, st));
+    MEQ_TRY(enqueue_stats(p, ws, k % 2 == 1, false, false, st));
     if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
       return MEQ_ERR_HIP;
     if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;

@@ -74,6 +74,12 @@ struct GemmGroup {
   int K;
   int tiles_m, tiles_n, tiles_per_mat;
   int tiles;           // batch * tiles_per_mat
+  // apply product only, when not null: sums of squares of the bf16 output per row of each
+  // 256-column tile (rpart, (L/256) x S per matrix) and per column of each 256-row tile
+  // (cpart, (S/256) x L per matrix), the partials of eq. "row-col-rms" for the last iteration
+  float* rpart;
+  float* cpart;
+  int64_t stride_rpart, stride_cpart;
 };
 
 struct GemmArgs {

@@ -184,10 +184,19 @@ def test_timing_events_report_every_kernel():
     run.step(LR)
     for kind in range(8):
         ms, n = run.upd.plan.get_timing(kind)
+        if kind == meq.K_ROWCOL:
+            # the step's row/column sums come from the last apply product's epilogue
+            assert n == 0, "rowcol"
+            continue
         assert n >= 1 and ms > 0, meq.KERNEL_NAMES[kind]
     ms, n = run.upd.plan.get_timing(meq.K_APPLY, reset=True)
     assert n == 5  # one apply launch per Newton-Schulz step for the single shape group
     assert run.upd.plan.get_timing(meq.K_APPLY) == (0.0, 0)
+    # the row/column sums kernel of its own still runs in the CV trace (no apply before X_0)
+    run.upd.plan.set_timing([meq.K_ROWCOL])
+    meq.ns_cv_trace(run.upd, [p.clone() for p in run.params], 1)
+    ms, n = run.upd.plan.get_timing(meq.K_ROWCOL, reset=True)
+    assert n >= 2 and ms > 0
 
 
 @pytest.mark.parametrize("name", ["llama-350m", "llama-1b", "llama-7b-block-x4"])
