@@ -254,3 +254,34 @@ def test_ns_cv_trace_rejects_bad_arguments_before_any_device_work():
     assert trace(r=None) == meq.MEQ_ERR_INVALID_ARG
     assert trace(w=0) == meq.MEQ_ERR_WORKSPACE
     assert trace(wb=ws - 1) == meq.MEQ_ERR_WORKSPACE
+
+
+def test_split_parameters_classifies_kinds():
+    import torch
+    from paper_2609_35701_amd.optim import split_parameters
+
+    class Tiny(torch.nn.Module):
+        def __init__(self, tied):
+            super().__init__()
+            self.embed = torch.nn.Embedding(50, 16)
+            self.q = torch.nn.Linear(16, 16, bias=False)
+            self.up = torch.nn.Linear(16, 40, bias=True)
+            self.norm = torch.nn.Parameter(torch.ones(16))
+            self.lm_head = torch.nn.Linear(16, 50, bias=False)
+            if tied:
+                self.lm_head.weight = self.embed.weight
+
+    hidden, aux, vec = split_parameters(Tiny(tied=False))
+    assert [tuple(p.shape) for p in hidden] == [(16, 16), (40, 16)]
+    assert [tuple(p.shape) for p in aux] == [(50, 16), (50, 16)]
+    assert sorted(tuple(p.shape) for p in vec) == [(16,), (40,)]
+    _, aux_t, _ = split_parameters(Tiny(tied=True))
+    assert len(aux_t) == 1  # a tied embedding / LM head is one parameter
+
+    class Conv(torch.nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.c = torch.nn.Conv2d(3, 4, 3)
+
+    with pytest.raises(ValueError):
+        split_parameters(Conv())
