@@ -9,8 +9,11 @@
 //
 // One workgroup = 4 waves = one 256 x 256 output tile; each wave owns a 128 x 128
 // quadrant as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation in AGPRs).
-// K advances in slabs of 32 through a 4-stage LDS ring (three slabs in flight while
-// one is consumed, which covers the latency of the loads that miss L2).  Global ->
+// K advances in slabs through an LDS ring.  The Gram and polynomial products use slabs of
+// 32 k in a 4-stage ring (three slabs in flight while one is consumed, which covers the
+// latency of the loads that miss L2 over their long K); the apply product uses slabs of
+// 64 k in a 2-stage ring (half the barriers, whole 128-byte rows of its NT operand per
+// fetch), which measures faster for it and slower for the Gram product.  Global ->
 // LDS traffic uses buffer loads that write LDS directly (no registers, no LDS store
 // instructions); 16-byte chunks are XOR-swizzled so fragment reads are free of bank
 // conflicts.  The epilogue stages the output tile (and, for P, the A tile it adds) in
@@ -35,9 +38,6 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
-constexpr int BK = 32;              // k per slab
-constexpr int kStageBytes = 32768;  // one ring stage: operand A slab (16 KiB) + operand B slab (16 KiB)
-constexpr int kDmaPerSlab = 8;      // LDS-bound buffer loads per wave per slab (4 per operand)
 // Buffer resource word 3 for raw (untyped, 32-bit format) buffer access on gfx9.
 constexpr int kBufferFlags = 0x00020000;
 
@@ -73,7 +73,8 @@ __device__ __forceinline__ void wait_vm() {
 // LDS layouts (bytes).  Each 16-lane pass of an LDS access covers 256 bytes (64 banks).
 //   NT slab (256 rows x 32 k):   row r at r * 64; 16-byte chunk c (k = 8c..8c+7) at slot c ^ ((r >> 2) & 3),
 //                                so 16 consecutive rows read at one chunk fill the 256 bytes exactly.
-//   NN slab (32 k x 256 n):      row k at k * 512; chunk c (n = 8c..8c+7) at slot c ^ (4 (k & 3)), so the
+//   NT slab (256 rows x 64 k):   row r at r * 128; chunk c at slot c ^ ((r >> 1) & 7), same property.
+//   NN slab (BK k x 256 n):      row k at k * 512; chunk c (n = 8c..8c+7) at slot c ^ (4 (k & 3)), so the
 //                                4 rows x 4 chunks a 32-lane transpose read touches fill 256 bytes exactly.
 //   staged output (256 x 256):   row r in ring stage r / 64 at (r % 64) * 512; chunk c at slot c ^ (r & 31).
 __device__ __forceinline__ int stage_byte(int rr, int c) {
@@ -107,18 +108,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   constexpr bool kNN = kMode == 2;
   constexpr bool kSym = kMode != 2;
   constexpr bool kHasE = kMode == 1;
-  // Four ring stages as separate objects, so the compiler can tell the stage being read
-  // from the stages being filled.
+  // Ring geometry: the apply product takes the wide slabs.
+  constexpr bool kWide = kNN;
+  constexpr int BK = kWide ? 64 : 32;                 // k per slab
+  constexpr int kStages = kWide ? 2 : 4;
+  constexpr int kStageBytes = kWide ? 65536 : 32768;  // operand A slab + operand B slab
+  constexpr int kOpBytes = kStageBytes / 2;
+  constexpr int kRowBytes = 2 * BK;                   // one NT slab row
+  constexpr int kDma = kWide ? 16 : 8;                // LDS-bound buffer loads per wave per slab
+  // Ring stages as separate objects, so the compiler can tell the stage being read from
+  // the stages being filled (the 2-stage ring leaves st2_ and st3_ unreferenced).
   __shared__ __attribute__((aligned(1024))) uint8_t st0_[kStageBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t st1_[kStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t st2_[kStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t st3_[kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st2_[kWide ? 16 : kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st3_[kWide ? 16 : kStageBytes];
   __shared__ float colsum_[kNN ? 4 : 1][256];  // apply: per-wave column partials of the fused sums
   lds_u8* const st0 = (lds_u8*)st0_;
   lds_u8* const st1 = (lds_u8*)st1_;
   lds_u8* const st2 = (lds_u8*)st2_;
   lds_u8* const st3 = (lds_u8*)st3_;
-  auto stage_of = [&](int q) { return q == 0 ? st0 : q == 1 ? st1 : q == 2 ? st2 : st3; };
+  // The epilogue stages 64-row quarters of the output tile, 32 KiB each.
+  auto stage_of = [&](int q) {
+    if constexpr (kWide)
+      return q == 0 ? st0 : q == 1 ? st0 + 32768 : q == 2 ? st1 : st1 + 32768;
+    else
+      return q == 0 ? st0 : q == 1 ? st1 : q == 2 ? st2 : st3;
+  };
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -165,14 +180,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int rowA0 = ti * 256;
   const int rowB0 = tj * 256;  // NT: operand-B rows; NN: output columns
 
-  // ---- global -> LDS slab loads: 4 instructions per wave per operand (1 KiB each).
-  // NT: instruction I = 4 wave + i covers rows 16I .. 16I + 15; lane -> row 16I + lane/4,
-  //     slot lane%4, which holds chunk slot ^ ((row >> 2) & 3) = slot ^ (lane >> 4).
-  const int nt_r = lane >> 2;
-  const int nt_c = (lane & 3) ^ (lane >> 4);
+  // ---- global -> LDS slab loads: kDma / 2 instructions per wave per operand (1 KiB each).
+  // NT: instruction I = (kDma / 2) wave + i covers R = 1024 / kRowBytes rows RI .. RI + R - 1;
+  //     lane -> row RI + lane / (64 / R), slot lane % (64 / R).  The slot holds chunk slot ^ swz:
+  //     64-byte rows:  swz = (row >> 2) & 3 = lane >> 4;
+  //     128-byte rows: swz = (row >> 1) & 7 = (lane >> 4) ^ 4 (I & 1).
+  constexpr int kRowsPerDma = 1024 / kRowBytes;
+  const int nt_r = lane / (kRowBytes / 16);
+  const int nt_c = (lane % (kRowBytes / 16)) ^ (lane >> 4);
   const int vA = 2 * ((rowA0 + nt_r) * lda + 8 * nt_c);
-  const int vB_nt = 2 * ((rowB0 + nt_r) * ldb + 8 * nt_c);
-  // NN: instruction I = 4 wave + i covers k rows 2I, 2I + 1; lane -> row 2I + lane/32, slot lane%32.
+  const int vA_odd = 2 * ((rowA0 + nt_r) * lda + 8 * (nt_c ^ 4));  // 128-byte rows, odd I
+  const int vB_nt = 2 * ((rowB0 + nt_r) * ldb + 8 * nt_c);         // 64-byte rows only
+  // NN: instruction I = (kDma / 2) wave + i covers k rows 2I, 2I + 1; lane -> row 2I + lane/32, slot lane%32.
   const int nn_r = lane >> 5;
   const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * (nn_r & 3))));
   const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * ((2 + nn_r) & 3))));
@@ -180,28 +199,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   auto issue_slab = [&](lds_u8* buf, int kt) {
     const int k0 = kt * BK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int I = 4 * wave + i;
-      dma16(rA, buf + I * 1024, vA, 2 * (16 * I * lda + k0));
+    for (int i = 0; i < kDma / 2; ++i) {
+      const int I = (kDma / 2) * wave + i;
+      dma16(rA, buf + I * 1024, (kWide && (i & 1)) ? vA_odd : vA, 2 * (kRowsPerDma * I * lda + k0));
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int I = 4 * wave + i;
+    for (int i = 0; i < kDma / 2; ++i) {
+      const int I = (kDma / 2) * wave + i;
       if (kNN)
-        dma16(rB, buf + 16384 + I * 1024, (i & 1) ? vB_nn1 : vB_nn0, 2 * ((k0 + 2 * I) * ldb));
+        dma16(rB, buf + kOpBytes + I * 1024, (i & 1) ? vB_nn1 : vB_nn0, 2 * ((k0 + 2 * I) * ldb));
       else
-        dma16(rB, buf + 16384 + I * 1024, vB_nt, 2 * (16 * I * ldb + k0));
+        dma16(rB, buf + kOpBytes + I * 1024, vB_nt, 2 * (kRowsPerDma * I * ldb + k0));
     }
   };
 
   // ---- fragment addresses (bytes within a stage)
   // NT fragment: row R = base + 32 i + lane%32 (base a multiple of 32), k chunk 2 kk + lane/32,
-  // at slot chunk ^ ((R >> 2) & 3) = chunk ^ ((lane >> 2) & 3).
-  const int offA = (wm * 128 + (lane & 31)) * 64;
-  const int offB_nt = 16384 + (wn * 128 + (lane & 31)) * 64;
-  int slot_kk[2];
+  // at slot chunk ^ swz(R), swz(R) = ((lane & 31) >> 2) & 3 (64-byte rows) or ((lane & 31) >> 1) & 7.
+  const int offA = (wm * 128 + (lane & 31)) * kRowBytes;
+  const int offB_nt = kOpBytes + (wn * 128 + (lane & 31)) * kRowBytes;
+  const int nt_swz = kWide ? ((lane & 31) >> 1) & 7 : ((lane & 31) >> 2) & 3;
+  int slot_kk[BK / 16];
 #pragma unroll
-  for (int kk = 0; kk < 2; ++kk) slot_kk[kk] = 16 * ((2 * kk + h) ^ ((lane >> 2) & 3));
+  for (int kk = 0; kk < BK / 16; ++kk) slot_kk[kk] = 16 * ((2 * kk + h) ^ nt_swz);
   // NN fragment via ds_read_b64_tr_b16: within each 16-lane group, lane q points at
   // k row q / 4 and n columns 4 (q % 4) .. +3; afterwards lane q holds 4 consecutive k
   // of column q, so two reads give the 8 k values an MFMA operand lane needs.
@@ -231,18 +251,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   auto load_frags = [&](const lds_u8* buf, int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[4]) {
     const int oa = offA + slot_kk[kk];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(buf + oa + i * 2048);
+    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(buf + oa + i * 32 * kRowBytes);
     if (kNN) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + (nn_off[j] + 16384 + 8192 * kk)));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + (nn_off[j] + 18432 + 8192 * kk)));
+        const i16x4 lo =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + (nn_off[j] + kOpBytes + 8192 * kk)));
+        const i16x4 hi =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + (nn_off[j] + kOpBytes + 2048 + 8192 * kk)));
         bfr[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
     } else {
       const int ob = offB_nt + slot_kk[kk];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const lds_bf16x8*>(buf + ob + j * 2048);
+      for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const lds_bf16x8*>(buf + ob + j * 32 * kRowBytes);
     }
   };
 
@@ -259,12 +281,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
   };
 
-  // Software pipeline over slabs (slab s lives in ring stage s % 4).  On entry to
-  // slab kt its first k step's fragments are already in registers (fa).  The wave reads
-  // the second step's fragments under the first step's MFMAs, then waits for its own
-  // loads of slab kt + 1 and meets the other waves: slab kt + 1 has fully landed and no
-  // wave reads slab kt's stage any more, so that stage is refilled with slab kt + 4 and
-  // slab kt + 1's first fragments are read under the second step's MFMAs.
+  // Software pipeline over slabs (slab s lives in ring stage s % kStages).  On entry to
+  // slab kt its first k step's fragments are already in registers (fa).  Each later step's
+  // fragments are read under the previous step's MFMAs.  Before the last step the wave waits
+  // for its own loads of slab kt + 1 and meets the other waves: slab kt + 1 has fully landed
+  // and no wave reads slab kt's stage any more, so that stage is refilled with slab
+  // kt + kStages and slab kt + 1's first fragments are read under the last step's MFMAs.
   const int nk = g.K / BK;
   bf16x8 fa[4], fb[4], ga[4], gb[4];
   auto bar = [] {
@@ -274,33 +296,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
   };
+  constexpr int kReads = kNN ? 12 : 8;  // LDS read instructions per k step
   auto slab = [&](lds_u8* cur, const lds_u8* nxt, int kt) {
     load_frags(cur, 1, ga, gb);
     mfma16(fa, fb);
-    sched_step<kNN ? 12 : 8, 0>();
+    sched_step<kReads, 0>();
+    if constexpr (kWide) {
+      load_frags(cur, 2, fa, fb);
+      mfma16(ga, gb);
+      sched_step<kReads, 0>();
+      load_frags(cur, 3, ga, gb);
+      mfma16(fa, fb);
+      sched_step<kReads, 0>();
+    }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave is done reading slab kt
-    wait_vm<2 * kDmaPerSlab>();          // this wave's loads of slab kt + 1 have landed
+    wait_vm<(kStages - 2) * kDma>();     // this wave's loads of slab kt + 1 have landed
     bar();
-    issue_slab(cur, min(kt + 4, nk - 1));  // past the end: a harmless reload of the last slab
+    issue_slab(cur, min(kt + kStages, nk - 1));  // past the end: a harmless reload of the last slab
     load_frags(nxt, 0, fa, fb);
     mfma16(ga, gb);
-    sched_step<kNN ? 12 : 8, kDmaPerSlab>();
+    sched_step<kReads, kDma>();
   };
 
-  // ---- main loop: four slabs per trip so every stage is addressed statically.
-  // K is a multiple of 256 (zero padding), so the slab count is a multiple of 8.
-  issue_slab(st0, 0);
-  issue_slab(st1, 1);
-  issue_slab(st2, 2);
-  issue_slab(st3, 3);
-  wait_vm<3 * kDmaPerSlab>();
-  bar();
-  load_frags(st0, 0, fa, fb);
-  for (int kt = 0; kt < nk; kt += 4) {
-    slab(st0, st1, kt);
-    slab(st1, st2, kt + 1);
-    slab(st2, st3, kt + 2);
-    slab(st3, st0, kt + 3);
+  // ---- main loop: kStages slabs per trip so every stage is addressed statically.
+  // K is a multiple of 256 (zero padding), so the slab count is a multiple of 4.
+  if constexpr (kWide) {
+    issue_slab(st0, 0);
+    issue_slab(st1, 1);
+    wait_vm<kDma>();
+    bar();
+    load_frags(st0, 0, fa, fb);
+    for (int kt = 0; kt < nk; kt += 2) {
+      slab(st0, st1, kt);
+      slab(st1, st0, kt + 1);
+    }
+  } else {
+    issue_slab(st0, 0);
+    issue_slab(st1, 1);
+    issue_slab(st2, 2);
+    issue_slab(st3, 3);
+    wait_vm<3 * kDma>();
+    bar();
+    load_frags(st0, 0, fa, fb);
+    for (int kt = 0; kt < nk; kt += 4) {
+      slab(st0, st1, kt);
+      slab(st1, st2, kt + 1);
+      slab(st2, st3, kt + 2);
+      slab(st3, st0, kt + 3);
+    }
   }
   wait_vm<0>();
   __syncthreads();
@@ -453,7 +496,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       const int cb = blk & 15, rb = blk >> 4;
       const int r0 = 32 * rb + 8 * g4;  // OUT rows r0 .. r0 + 7 (one stage)
       const int c0 = 16 * cb;
-      const lds_u8* src = r0 < 64 ? st0 : r0 < 128 ? st1 : r0 < 192 ? st2 : st3;
+      const lds_u8* src = stage_of(r0 >> 6);
       u32x4 out;
 #pragma unroll
       for (int t4 = 0; t4 < 2; ++t4) {
