@@ -138,6 +138,63 @@ def summarize_stats(stats_csv: str, out: str, command: str, note: str) -> None:
         f.write("".join(lines))
 
 
+MFMA_COUNTERS = ("GRBM_GUI_ACTIVE", "SQ_BUSY_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+SIMDS = 256 * 4  # MI355X: 256 compute units of 4 SIMDs
+XCDS = 8
+
+
+def ns_launch_flops(wl) -> dict:
+    """Per launch of each NS product over all shape groups: (algorithmic symmetric-aware flops,
+    flops the 256 x 256 tiles execute, padding and the lower half of diagonal tiles included)."""
+    out = {"k_ns_gemm<0>": [0, 0], "k_ns_gemm<1>": [0, 0], "k_ns_gemm<2>": [0, 0]}
+    for m in wl.matrices:
+        s, l = min(m.rows, m.cols), max(m.rows, m.cols)
+        sp, lp = -(-s // 256) * 256, -(-l // 256) * 256
+        tm, tl = sp // 256, lp // 256
+        tri = tm * (tm + 1) // 2
+        for k, alg, exe in (("k_ns_gemm<0>", s * s * l, tri * 2 * 256 * 256 * lp),
+                            ("k_ns_gemm<1>", s ** 3, tri * 2 * 256 * 256 * sp),
+                            ("k_ns_gemm<2>", 2 * s * s * l, tm * tl * 2 * 256 * 256 * sp)):
+            out[k][0] += alg
+            out[k][1] += exe
+    return out
+
+
+def summarize_mfma(run_dir: str, out: str, command: str, workload: str, note: str) -> None:
+    """Matrix-core utilisation of the NS products from one rocprofv3 --pmc run of MFMA_COUNTERS."""
+    import workloads
+
+    wl = workloads.workload(workload)
+    flops = ns_launch_flops(wl)
+    means = {c: _counter_means(run_dir, c) for c in MFMA_COUNTERS}
+    lines = [
+        f"# Matrix-core counters of the Newton-Schulz products, {workload} step\n\n",
+        "Command (from the repository root on one MI355X):\n\n", f"    {command}\n\n",
+        f"Summarised with `python bench.py --summarize-mfma <dir> --out <this file>`.  Per dispatch: "
+        "GRBM_GUI_ACTIVE summed over the 8 XCDs (divided by 8: cycles the kernel was active); "
+        f"SQ_VALU_MFMA_BUSY_CYCLES summed over all {SIMDS} SIMDs (divided by {SIMDS} and by the active cycles: "
+        "fraction of the time a SIMD's matrix core was busy); SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 = bf16 "
+        "flops the matrix cores executed, against the flops the 256 x 256 tiles execute by count "
+        "(padding and the lower half of diagonal tiles of the symmetric products included) and the "
+        "algorithmic symmetric-aware flops.\n\n",
+        (note + "\n\n" if note else ""),
+        "| kernel | dispatches | active cycles | MFMA busy | MOPS x 512 | tile flops | algorithmic flops | "
+        "MOPS x 512 / tile flops |\n",
+        "|---|---|---|---|---|---|---|---|\n",
+    ]
+    for k in ("k_ns_gemm<0>", "k_ns_gemm<1>", "k_ns_gemm<2>"):
+        gui, n = means["GRBM_GUI_ACTIVE"].get(k, (float("nan"), 0))
+        cyc = gui / XCDS
+        busy = means["SQ_VALU_MFMA_BUSY_CYCLES"].get(k, (float("nan"), 0))[0] / SIMDS / cyc
+        mops = means["SQ_INSTS_VALU_MFMA_MOPS_BF16"].get(k, (float("nan"), 0))[0] * 512
+        alg, exe = flops[k]
+        lines.append(f"| {k} | {n} | {cyc:.4g} | {busy:.1%} | {mops:.4g} | {exe:.4g} | {alg:.4g} | "
+                     f"{mops / exe:.4f} |\n")
+    lines.append(f"\nkernel_source_sha256: {gemm_source_hash()}\n")
+    with open(out, "w") as f:
+        f.write("".join(lines))
+
+
 def ns_flops(s: int, l: int, steps: int):
     """Algorithmic Newton-Schulz flops of one matrix: (symmetric-aware total, apply-only, dense total)."""
     sym = steps * (3 * s * s * l + s ** 3)
@@ -282,6 +339,8 @@ def main() -> int:
                     help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) into --out and exit")
     ap.add_argument("--summarize-stats", metavar="STATS_CSV",
                     help="summarise a rocprofv3 --kernel-trace --stats run into --out and exit")
+    ap.add_argument("--summarize-mfma", metavar="PMC_DIR",
+                    help="summarise a rocprofv3 --pmc run of the matrix-core counters into --out and exit")
     ap.add_argument("--out")
     ap.add_argument("--command", default="", help="command line(s) recorded in a summary ('|' separates two)")
     ap.add_argument("--note", default="")
@@ -293,6 +352,9 @@ def main() -> int:
         return 0
     if args.summarize_stats:
         summarize_stats(args.summarize_stats, args.out, args.command, args.note)
+        return 0
+    if args.summarize_mfma:
+        summarize_mfma(args.summarize_mfma, args.out, args.command, args.workload, args.note)
         return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the MeqMuon update is measured on a single MI355X; "
