@@ -282,6 +282,41 @@ def extras_leg(params, wl, lr: float, steps: int, warmup: int) -> dict:
     return out
 
 
+def library_gemm_leg() -> dict:
+    """The platform's library GEMM (hipBLASLt through torch.bmm / torch.mm) on the apply
+    product's largest shape group of the 1B step (48 x (2048 x 2048 @ 2048 x 8192), bf16 in and
+    out) and on one large square product: what a tuned dense kernel reaches on this chip under
+    the same clock and power limits."""
+    import torch
+
+    dev = torch.device("cuda:0")
+    out = {}
+
+    def rate(f, flops, iters):
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / iters
+        return {"ms": ms, "tflops": flops / (ms * 1e-3) / 1e12}
+
+    p = torch.randn(48, 2048, 2048, device=dev, dtype=torch.bfloat16)
+    x = torch.randn(48, 2048, 8192, device=dev, dtype=torch.bfloat16)
+    out["bmm_48x2048x2048x8192"] = rate(lambda: torch.bmm(p, x), 2.0 * 48 * 2048 * 2048 * 8192, 10)
+    del p, x
+    a = torch.randn(8192, 8192, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(8192, 8192, device=dev, dtype=torch.bfloat16)
+    out["mm_8192_cubed"] = rate(lambda: torch.mm(a, b), 2.0 * 8192 ** 3, 10)
+    del a, b
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline_leg(wl, lr: float, budget_s: float):
     """Time the fp64 oracle on one matrix of each distinct shape and scale to a whole step."""
     import numpy as np
@@ -438,6 +473,7 @@ def main() -> int:
         print("# bench: other parameter kinds and the Moonlight-Muon rule", file=sys.stderr, flush=True)
         extras = extras_leg(params, wl, args.lr, min(args.steps, 20), max(args.warmup, 1))
         extras["equilibration_overhead_ms"] = ms_per_step - extras["moonlight_hidden"]["ms_per_step"]
+        extras["library_gemm"] = library_gemm_leg()
     cpu = None
     if not args.no_cpu_baseline:
         print("# bench: timing the fp64 oracle on host cores", file=sys.stderr, flush=True)

@@ -199,7 +199,7 @@ def test_timing_events_report_every_kernel():
     assert n >= 2 and ms > 0
 
 
-@pytest.mark.parametrize("name", ["llama-350m", "llama-1b", "llama-7b-block-x4"])
+@pytest.mark.parametrize("name", ["llama-130m", "llama-350m", "llama-1b", "llama-7b-block-x4"])
 def test_full_launch_sampled_parity(name):
     """A full-size workload in one meq_step (the 1B one is the benchmark's launch
     configuration; the 7B block carries the extreme row/column imbalance); the first and last
