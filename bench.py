@@ -353,7 +353,45 @@ def cpu_baseline_leg(wl, lr: float, budget_s: float):
     return {"value": 1.0 / sec_per_step, "unit": "steps/s", "cores": threads, "kind": "oracle",
             "sample": f"fp64 numpy oracle, one matrix of each shape timed once (wide-orientation NS), "
                       f"scaled by shape counts to the full {wl.count}-matrix step: {sample}; "
-                      f"est. {sec_per_step:.1f} s/step"}
+                      f"est. {sec_per_step:.1f} s/step",
+            "affinity_cores": len(os.sched_getaffinity(0)), "blas_threads": threads,
+            "single_core": single_core_leg(lr)}
+
+
+def single_core_leg(lr: float) -> dict:
+    """The oracle with BLAS limited to one thread: the single 256 x 512 fp32 step whole, and the
+    130M-shape step estimated from one matrix of each shape."""
+    import numpy as np
+
+    import oracle
+    import workloads
+
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        return None
+    hp = oracle.HParams()
+    out = {}
+    with threadpool_limits(limits=1, user_api="blas"):
+        wl = workloads.workload("single-256x512")
+        w0 = workloads.weight_init(wl, 0).astype(np.float64)
+        g = workloads.grad_at_step(wl, 0, 0).astype(np.float64)
+        t0 = time.perf_counter()
+        oracle.meq_step(w0, g, np.zeros_like(w0), hp, lr)
+        out["single-256x512_s_per_step"] = time.perf_counter() - t0
+        wl = workloads.workload("llama-130m")
+        first = {}
+        for i, m in enumerate(wl.matrices):
+            first.setdefault((m.rows, m.cols), []).append(i)
+        est = 0.0
+        for idxs in first.values():
+            w0 = workloads.weight_init(wl, idxs[0]).astype(np.float64)
+            g = workloads.grad_at_step(wl, idxs[0], 0).astype(np.float64)
+            t0 = time.perf_counter()
+            oracle.meq_step(w0, g, np.zeros_like(w0), hp, lr, wide=True)
+            est += (time.perf_counter() - t0) * len(idxs)
+        out["llama-130m_s_per_step_est"] = est
+    return out
 
 
 def main() -> int:

@@ -202,15 +202,16 @@ def test_timing_events_report_every_kernel():
 @pytest.mark.parametrize("name", ["llama-130m", "llama-350m", "llama-1b", "llama-7b-block-x4"])
 def test_full_launch_sampled_parity(name):
     """A full-size workload in one meq_step (the 1B one is the benchmark's launch
-    configuration; the 7B block carries the extreme row/column imbalance); the first and last
-    matrix of each shape group are seeded from the numpy generator and checked against the
+    configuration; the 7B block carries the extreme row/column imbalance); the first, middle and
+    last matrix of each shape group are seeded from the numpy generator and checked against the
     oracle, the rest carry device-drawn inputs of the same recipe."""
     wl = workloads.workload(name)
     shapes = [(m.rows, m.cols) for m in wl.matrices]
     groups = {}
     for i, s in enumerate(shapes):
         groups.setdefault((min(s), max(s)), []).append(i)
-    sample = sorted({g[0] for g in groups.values()} | {g[-1] for g in groups.values()})
+    sample = sorted({g[0] for g in groups.values()} | {g[len(g) // 2] for g in groups.values()} |
+                    {g[-1] for g in groups.values()})
     log(f"[case] {name} full launch, sampled matrices {sample}")
     params, grads, _ = workloads.device_inputs(wl, DEV)
     w_np, g_np = {}, {}
