@@ -52,7 +52,9 @@ typedef enum {
   MEQ_ERR_INVALID_ARG = -1, /* a null pointer, a bad size or hyperparameter, a count mismatch   */
   MEQ_ERR_UNSUPPORTED = -2, /* a dtype combination or size the library does not implement        */
   MEQ_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed                          */
-  MEQ_ERR_WORKSPACE = -4    /* the workspace is null, too small or not 256-byte aligned           */
+  MEQ_ERR_WORKSPACE = -4,   /* the workspace is null, too small or not 256-byte aligned           */
+  MEQ_ERR_NO_MEMORY = -5    /* a host allocation (plan metadata, launch lists) failed; no launch   */
+                            /* of the failing call was enqueued after the failure                  */
 } meq_status;
 
 typedef enum { MEQ_F32 = 0, MEQ_BF16 = 1 } meq_dtype;

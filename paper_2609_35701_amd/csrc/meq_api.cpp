@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstring>
 #include <map>
+#include <memory>
 #include <new>
 #include <utility>
 #include <vector>
@@ -116,6 +117,7 @@ meq_status timed_launch(meq_plan* p, int kind, hipStream_t st, F&& fn) {
   const bool timed = (p->timing_mask >> kind) & 1u;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (timed) {
+    p->pending.reserve(p->pending.size() + 1);  // may throw: before anything is recorded
     e0 = take_event(p);
     e1 = take_event(p);
     if (!e0 || !e1 || hipEventRecord(e0, st) != hipSuccess) return MEQ_ERR_HIP;
@@ -133,6 +135,18 @@ meq_status timed_launch(meq_plan* p, int kind, hipStream_t st, F&& fn) {
     const meq_status _s = (expr);     \
     if (_s != MEQ_OK) return _s;      \
   } while (0)
+
+// Exported calls keep C++ exceptions (host allocations) on this side of the C ABI.
+template <typename F>
+meq_status guarded(F&& fn) {
+  try {
+    return fn();
+  } catch (const std::bad_alloc&) {
+    return MEQ_ERR_NO_MEMORY;
+  } catch (...) {
+    return MEQ_ERR_INVALID_ARG;
+  }
+}
 
 }  // namespace
 
@@ -158,6 +172,7 @@ MEQ_EXPORT const char* meq_status_string(meq_status s) {
     case MEQ_ERR_UNSUPPORTED: return "unsupported dtype or size";
     case MEQ_ERR_HIP: return "HIP runtime error";
     case MEQ_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+    case MEQ_ERR_NO_MEMORY: return "host memory allocation failed";
   }
   return "unknown status";
 }
@@ -174,7 +189,8 @@ meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hpa
     if (S * L * 2 > kMaxWideBytes) return MEQ_ERR_UNSUPPORTED;
   }
   meq_plan* p = new (std::nothrow) meq_plan();
-  if (!p) return MEQ_ERR_INVALID_ARG;
+  if (!p) return MEQ_ERR_NO_MEMORY;
+  std::unique_ptr<meq_plan> owner(p);  // freed if an allocation below throws
   p->hp = *hp;
   p->mats.resize(count);
   std::map<std::pair<int64_t, int64_t>, int> group_of;
@@ -245,7 +261,7 @@ meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hpa
     off = align_up(off + 4 * static_cast<size_t>(std::max(mi.m, mi.n)), kAlign);
   }
   p->ws_bytes = off;
-  *out = p;
+  *out = owner.release();
   return MEQ_OK;
 }
 
@@ -261,7 +277,8 @@ meq_status init_stream_kind(int32_t kind, const meq_matrix_desc* mats, int32_t c
     MEQ_TRY(validate_dtypes(d));
   }
   meq_plan* p = new (std::nothrow) meq_plan();
-  if (!p) return MEQ_ERR_INVALID_ARG;
+  if (!p) return MEQ_ERR_NO_MEMORY;
+  std::unique_ptr<meq_plan> owner(p);
   p->kind = kind;
   p->hp = *hp;
   p->mats.resize(count);
@@ -291,7 +308,7 @@ meq_status init_stream_kind(int32_t kind, const meq_matrix_desc* mats, int32_t c
     }
   }
   p->ws_bytes = off;
-  *out = p;
+  *out = owner.release();
   return MEQ_OK;
 }
 
@@ -304,8 +321,9 @@ MEQ_EXPORT meq_status meq_init_kind(int32_t kind, const meq_matrix_desc* mats, i
   if (kind != MEQ_PARAM_HIDDEN && kind != MEQ_PARAM_AUX && kind != MEQ_PARAM_VECTOR) return MEQ_ERR_INVALID_ARG;
   MEQ_TRY(validate_hparams(*hp));
   if (hp->update_rule != MEQ_RULE_MEQMUON && kind != MEQ_PARAM_HIDDEN) return MEQ_ERR_INVALID_ARG;
-  if (kind == MEQ_PARAM_HIDDEN) return init_hidden(mats, count, hp, out);
-  return init_stream_kind(kind, mats, count, hp, out);
+  return guarded([&] {
+    return kind == MEQ_PARAM_HIDDEN ? init_hidden(mats, count, hp, out) : init_stream_kind(kind, mats, count, hp, out);
+  });
 }
 
 MEQ_EXPORT meq_status meq_init(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out) {
@@ -733,16 +751,18 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     return MEQ_ERR_WORKSPACE;
 
   char* ws = static_cast<char*>(workspace);
-  if (p->kind == MEQ_PARAM_AUX) return step_aux(p, params, grads, momenta, lr, ws, st);
-  if (p->kind == MEQ_PARAM_VECTOR) return step_vec(p, params, grads, momenta, lr, ws, st);
-  const meq_hparams& hp = p->hp;
-  const bool moonlight = hp.update_rule == MEQ_RULE_MOONLIGHT;
-  MEQ_TRY(enqueue_prescale(p, ws, grads, momenta, st));
-  for (int k = 0; k < hp.ns_steps; ++k)
-    MEQ_TRY(enqueue_ns_iteration(p, ws, k, !moonlight && k == hp.ns_steps - 1, st));
-  MEQ_TRY(enqueue_stats(p, ws, hp.ns_steps % 2 == 1, moonlight, !moonlight, st));
-  MEQ_TRY(enqueue_update(p, ws, params, lr, st));
-  return MEQ_OK;
+  return guarded([&]() -> meq_status {
+    if (p->kind == MEQ_PARAM_AUX) return step_aux(p, params, grads, momenta, lr, ws, st);
+    if (p->kind == MEQ_PARAM_VECTOR) return step_vec(p, params, grads, momenta, lr, ws, st);
+    const meq_hparams& hp = p->hp;
+    const bool moonlight = hp.update_rule == MEQ_RULE_MOONLIGHT;
+    MEQ_TRY(enqueue_prescale(p, ws, grads, momenta, st));
+    for (int k = 0; k < hp.ns_steps; ++k)
+      MEQ_TRY(enqueue_ns_iteration(p, ws, k, !moonlight && k == hp.ns_steps - 1, st));
+    MEQ_TRY(enqueue_stats(p, ws, hp.ns_steps % 2 == 1, moonlight, !moonlight, st));
+    MEQ_TRY(enqueue_update(p, ws, params, lr, st));
+    return MEQ_OK;
+  });
 }
 
 MEQ_EXPORT meq_status meq_ns_cv_trace(meq_plan* p, const void* const* inputs, int32_t kmax, void* workspace,
@@ -756,22 +776,24 @@ MEQ_EXPORT meq_status meq_ns_cv_trace(meq_plan* p, const void* const* inputs, in
   if (!workspace || workspace_bytes < p->ws_bytes || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
     return MEQ_ERR_WORKSPACE;
   char* ws = static_cast<char*>(workspace);
-  std::vector<MatScalars> host(count);
-  const char* src = ws + p->off_scal;
-  MEQ_TRY(enqueue_prescale(p, ws, inputs, nullptr, st));
-  for (int k = 0; k <= kmax; ++k) {
-    if (k > 0) MEQ_TRY(enqueue_ns_iteration(p, ws, k - 1, false, st));
-    // X_0 (unscaled V: CVs are scale free) sits in buffer a; iteration k - 1 writes b for odd k
-    MEQ_TRY(enqueue_stats(p, ws, k % 2 == 1, false, false, st));
-    if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
-      return MEQ_ERR_HIP;
-    if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;
-    for (int i = 0; i < count; ++i) {
-      gamma_r[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_r;
-      gamma_c[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_c;
+  return guarded([&]() -> meq_status {
+    std::vector<MatScalars> host(count);
+    const char* src = ws + p->off_scal;
+    MEQ_TRY(enqueue_prescale(p, ws, inputs, nullptr, st));
+    for (int k = 0; k <= kmax; ++k) {
+      if (k > 0) MEQ_TRY(enqueue_ns_iteration(p, ws, k - 1, false, st));
+      // X_0 (unscaled V: CVs are scale free) sits in buffer a; iteration k - 1 writes b for odd k
+      MEQ_TRY(enqueue_stats(p, ws, k % 2 == 1, false, false, st));
+      if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
+        return MEQ_ERR_HIP;
+      if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;
+      for (int i = 0; i < count; ++i) {
+        gamma_r[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_r;
+        gamma_c[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_c;
+      }
     }
-  }
-  return MEQ_OK;
+    return MEQ_OK;
+  });
 }
 
 MEQ_EXPORT meq_status meq_get_stats(const meq_plan* plan, const void* workspace, double* gamma_r, double* gamma_c,
@@ -781,17 +803,19 @@ MEQ_EXPORT meq_status meq_get_stats(const meq_plan* plan, const void* workspace,
   const size_t count = plan->mats.size();
   if (count == 0) return MEQ_OK;
   if (!workspace) return MEQ_ERR_WORKSPACE;
-  std::vector<MatScalars> host(count);
-  const char* src = static_cast<const char*>(workspace) + plan->off_scal;
-  if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
-    return MEQ_ERR_HIP;
-  if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;
-  for (size_t i = 0; i < count; ++i) {
-    if (gamma_r) gamma_r[i] = host[i].gamma_r;
-    if (gamma_c) gamma_c[i] = host[i].gamma_c;
-    if (dir) dir[i] = host[i].dir;
-  }
-  return MEQ_OK;
+  return guarded([&]() -> meq_status {
+    std::vector<MatScalars> host(count);
+    const char* src = static_cast<const char*>(workspace) + plan->off_scal;
+    if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
+      return MEQ_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;
+    for (size_t i = 0; i < count; ++i) {
+      if (gamma_r) gamma_r[i] = host[i].gamma_r;
+      if (gamma_c) gamma_c[i] = host[i].gamma_c;
+      if (dir) dir[i] = host[i].dir;
+    }
+    return MEQ_OK;
+  });
 }
 
 MEQ_EXPORT meq_status meq_set_timing(meq_plan* plan, uint32_t kind_mask) {
@@ -803,16 +827,25 @@ MEQ_EXPORT meq_status meq_set_timing(meq_plan* plan, uint32_t kind_mask) {
 MEQ_EXPORT meq_status meq_get_timing(meq_plan* plan, int32_t kind, double* total_ms, int64_t* launches,
                                      int32_t reset) {
   if (!plan || kind < 0 || kind >= MEQ_K_COUNT) return MEQ_ERR_INVALID_ARG;
-  for (const TimedLaunch& tl : plan->pending) {
-    if (hipEventSynchronize(tl.stop) != hipSuccess) return MEQ_ERR_HIP;
-    float ms = 0.f;
-    if (hipEventElapsedTime(&ms, tl.start, tl.stop) != hipSuccess) return MEQ_ERR_HIP;
-    plan->total_ms[tl.kind] += ms;
-    plan->launches[tl.kind] += 1;
-    plan->event_pool.push_back(tl.start);
-    plan->event_pool.push_back(tl.stop);
-  }
-  plan->pending.clear();
+  // Fold the finished launches into the totals; on an error the launches already folded
+  // are dropped from the pending list, so a later call does not count them twice.
+  size_t done = 0;
+  meq_status status = guarded([&]() -> meq_status {
+    for (; done < plan->pending.size(); ++done) {
+      const TimedLaunch& tl = plan->pending[done];
+      if (hipEventSynchronize(tl.stop) != hipSuccess) return MEQ_ERR_HIP;
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, tl.start, tl.stop) != hipSuccess) return MEQ_ERR_HIP;
+      plan->event_pool.reserve(plan->event_pool.size() + 2);
+      plan->total_ms[tl.kind] += ms;
+      plan->launches[tl.kind] += 1;
+      plan->event_pool.push_back(tl.start);
+      plan->event_pool.push_back(tl.stop);
+    }
+    return MEQ_OK;
+  });
+  plan->pending.erase(plan->pending.begin(), plan->pending.begin() + static_cast<std::ptrdiff_t>(done));
+  if (status != MEQ_OK) return status;
   if (total_ms) *total_ms = plan->total_ms[kind];
   if (launches) *launches = plan->launches[kind];
   if (reset) {
