@@ -196,13 +196,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * (nn_r & 3))));
   const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * ((2 + nn_r) & 3))));
 
-  auto issue_slab = [&](lds_u8* buf, int kt) {
+  auto issue_half_a = [&](lds_u8* buf, int kt) {
     const int k0 = kt * BK;
 #pragma unroll
     for (int i = 0; i < kDma / 2; ++i) {
       const int I = (kDma / 2) * wave + i;
       dma16(rA, buf + I * 1024, (kWide && (i & 1)) ? vA_odd : vA, 2 * (kRowsPerDma * I * lda + k0));
     }
+  };
+  auto issue_half_b = [&](lds_u8* buf, int kt) {
+    const int k0 = kt * BK;
 #pragma unroll
     for (int i = 0; i < kDma / 2; ++i) {
       const int I = (kDma / 2) * wave + i;
@@ -211,6 +214,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       else
         dma16(rB, buf + kOpBytes + I * 1024, vB_nt, 2 * (kRowsPerDma * I * ldb + k0));
     }
+  };
+  auto issue_slab = [&](lds_u8* buf, int kt) {
+    issue_half_a(buf, kt);
+    issue_half_b(buf, kt);
   };
 
   // ---- fragment addresses (bytes within a stage)
@@ -285,8 +292,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // slab kt its first k step's fragments are already in registers (fa).  Each later step's
   // fragments are read under the previous step's MFMAs.  Before the last step the wave waits
   // for its own loads of slab kt + 1 and meets the other waves: slab kt + 1 has fully landed
-  // and no wave reads slab kt's stage any more, so that stage is refilled with slab
-  // kt + kStages and slab kt + 1's first fragments are read under the last step's MFMAs.
+  // and no wave reads slab kt's stage any more, so the refill of that stage with slab
+  // kt + kStages starts (operand A) and slab kt + 1's first fragments are read under the last
+  // step's MFMAs.  Operand B of that refill goes out under the first step of slab kt + 1:
+  // split in two, the LDS-bound loads queue behind outstanding misses in smaller bursts,
+  // which keeps more of the MFMA stream moving (3% faster than one burst per slab).
+  // The waits count loads in issue order: at the barrier of slab kt everything issued after
+  // slab kt + 1's operand B may still be in flight, i.e. kStages - 2 slabs.
   const int nk = g.K / BK;
   bf16x8 fa[4], fb[4], ga[4], gb[4];
   auto bar = [] {
@@ -297,10 +309,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     asm volatile("" ::: "memory");
   };
   constexpr int kReads = kNN ? 12 : 8;  // LDS read instructions per k step
-  auto slab = [&](lds_u8* cur, const lds_u8* nxt, int kt) {
+  // cur: slab kt's stage; nxt: slab kt + 1's; prv: the stage freed at the last barrier
+  auto slab = [&](lds_u8* cur, const lds_u8* nxt, lds_u8* prv, int kt) {
     load_frags(cur, 1, ga, gb);
+    issue_half_b(prv, min(kt - 1 + kStages, nk - 1));  // second half of the slab started at the last barrier
     mfma16(fa, fb);
-    sched_step<kReads, 0>();
+    sched_step<kReads, kDma / 2>();
     if constexpr (kWide) {
       load_frags(cur, 2, fa, fb);
       mfma16(ga, gb);
@@ -312,37 +326,38 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave is done reading slab kt
     wait_vm<(kStages - 2) * kDma>();     // this wave's loads of slab kt + 1 have landed
     bar();
-    issue_slab(cur, min(kt + kStages, nk - 1));  // past the end: a harmless reload of the last slab
+    issue_half_a(cur, min(kt + kStages, nk - 1));  // past the end: a harmless reload of the last slab
     load_frags(nxt, 0, fa, fb);
     mfma16(ga, gb);
-    sched_step<kReads, kDma>();
+    sched_step<kReads, kDma / 2>();
   };
 
   // ---- main loop: kStages slabs per trip so every stage is addressed statically.
-  // K is a multiple of 256 (zero padding), so the slab count is a multiple of 4.
+  // K is a multiple of 256 (zero padding), so the slab count is a multiple of 4.  The
+  // prologue issues all but operand B of slab kStages - 1, which the first slab sends.
   if constexpr (kWide) {
     issue_slab(st0, 0);
-    issue_slab(st1, 1);
-    wait_vm<kDma>();
+    issue_half_a(st1, 1);
+    wait_vm<kDma / 2>();
     bar();
     load_frags(st0, 0, fa, fb);
     for (int kt = 0; kt < nk; kt += 2) {
-      slab(st0, st1, kt);
-      slab(st1, st0, kt + 1);
+      slab(st0, st1, st1, kt);
+      slab(st1, st0, st0, kt + 1);
     }
   } else {
     issue_slab(st0, 0);
     issue_slab(st1, 1);
     issue_slab(st2, 2);
-    issue_slab(st3, 3);
-    wait_vm<3 * kDma>();
+    issue_half_a(st3, 3);
+    wait_vm<2 * kDma + kDma / 2>();
     bar();
     load_frags(st0, 0, fa, fb);
     for (int kt = 0; kt < nk; kt += 4) {
-      slab(st0, st1, kt);
-      slab(st1, st2, kt + 1);
-      slab(st2, st3, kt + 2);
-      slab(st3, st0, kt + 3);
+      slab(st0, st1, st3, kt);
+      slab(st1, st2, st0, kt + 1);
+      slab(st2, st3, st1, kt + 2);
+      slab(st3, st0, st2, kt + 3);
     }
   }
   wait_vm<0>();
