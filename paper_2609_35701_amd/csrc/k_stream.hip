@@ -80,7 +80,12 @@ __device__ __forceinline__ uint4 pack_bf16x8(const uint16_t (&h)[8]) {
 // into the zero-padded wide buffer (transposed through LDS for tall matrices).
 // Without a momentum buffer (b == nullptr) V is the input G itself.
 // One block = one 64 x 128 tile of the padded matrix in its own orientation;
-// thread (ty, tx) owns rows ty + 16 k (k < 4) and columns 8 tx .. 8 tx + 7.
+// thread (ty, tx) owns columns 8 tx .. 8 tx + 7 of rows ty + 16 k (wide) or of the four
+// consecutive rows 4 ty + k (tall, k < 4).
+// Tall tiles pass through LDS as tr[own column][own row]: a thread writes the four rows of
+// one column as one 8-byte chunk, and each 128-byte row of tr holds its 8-byte chunks at
+// chunk ^ 2 ((column >> 3) & 7), which spreads a wave's writes evenly over the banks and
+// keeps the 16-byte pairs the read-back takes adjacent.
 template <bool kGradBf16>
 __global__ __launch_bounds__(256) void k_momentum(MomentumArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t tr[kEwCols][kEwRows + 8];  // tall: [own column][own row]
@@ -98,9 +103,10 @@ __global__ __launch_bounds__(256) void k_momentum(MomentumArgs a) {
   const float mu = a.mu;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   float ss = 0.f;
+  uint16_t hv[8][4];  // tall: column q, rows 4 ty + k
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const int row = r0 + ty + 16 * k;
+    const int row = r0 + (tall ? 4 * ty + k : ty + 16 * k);
     const int col = c0 + 8 * tx;
     float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (row < m && col < n) {
@@ -149,18 +155,26 @@ __global__ __launch_bounds__(256) void k_momentum(MomentumArgs a) {
       *reinterpret_cast<uint4*>(xp + static_cast<int64_t>(row) * ldx + col) = pack_bf16x8(h);
     } else {
 #pragma unroll
-      for (int q = 0; q < 8; ++q) tr[8 * tx + q][ty + 16 * k] = h[q];
+      for (int q = 0; q < 8; ++q) hv[q][k] = h[q];
     }
   }
   if (tall) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int c = 8 * tx + q;  // local own-column index; its rows 4 ty .. 4 ty + 3 form chunk ty
+      uint2 w;
+      w.x = hv[q][0] | (static_cast<uint32_t>(hv[q][1]) << 16);
+      w.y = hv[q][2] | (static_cast<uint32_t>(hv[q][3]) << 16);
+      *reinterpret_cast<uint2*>(&tr[c][4 * (ty ^ (2 * (tx & 7)))]) = w;
+    }
     __syncthreads();
     // wide row = own column (128 of them), wide column = own row (64): 8 threads per wide row
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int wr = (threadIdx.x >> 3) + 32 * k;  // local own-column index
-      const int wc = 8 * (threadIdx.x & 7);        // local own-row index
-      const uint4 pk = *reinterpret_cast<const uint4*>(&tr[wr][wc]);
-      *reinterpret_cast<uint4*>(xp + static_cast<int64_t>(c0 + wr) * ldx + r0 + wc) = pk;
+      const int j = threadIdx.x & 7;               // own rows 8 j .. 8 j + 7
+      const uint4 pk = *reinterpret_cast<const uint4*>(&tr[wr][8 * (j ^ ((wr >> 3) & 7))]);
+      *reinterpret_cast<uint4*>(xp + static_cast<int64_t>(c0 + wr) * ldx + r0 + 8 * j) = pk;
     }
   }
   const float tot = block_sum256(ss, red);
@@ -306,8 +320,9 @@ __global__ __launch_bounds__(256) void k_select(SelectArgs a) {
 
 // --------------------------------------------------------------------------------
 // W <- decay * W - step * U * scale over 64 x 128 tiles of the matrix's own orientation
-// (thread (ty, tx): rows ty + 16 k, columns 8 tx .. 8 tx + 7); U is read from the padded
-// wide buffer (staged through LDS and transposed for tall matrices).
+// (thread (ty, tx): columns 8 tx .. 8 tx + 7 of rows ty + 16 k, or of rows 4 ty + k for tall
+// matrices); U is read from the padded wide buffer (staged through LDS and transposed for
+// tall matrices, in the momentum kernel's swizzled layout).
 template <bool kParamBf16>
 __global__ __launch_bounds__(256) void k_update(UpdateArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t tr[kEwCols][kEwRows + 8];  // tall: [own column][own row]
@@ -323,16 +338,20 @@ __global__ __launch_bounds__(256) void k_update(UpdateArgs a) {
   const float* __restrict__ scale = a.scale[mi];
   const int dir = a.scal[mi]->dir;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  uint2 tch[8];  // tall: own rows 4 ty .. 4 ty + 3 of column 8 tx + q
   if (tall) {
-    // own rows r0.., cols c0.. = wide rows c0.., wide cols r0..  (the wide buffer is padded: no bounds)
+    // own rows r0.., cols c0.. = wide rows c0.., wide cols r0..  (the wide buffer is padded: no
+    // bounds); the same swizzled layout as the momentum kernel's transpose
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int wr = (threadIdx.x >> 3) + 32 * k;
-      const int wc = 8 * (threadIdx.x & 7);
-      const uint4 pk = *reinterpret_cast<const uint4*>(u + static_cast<int64_t>(c0 + wr) * ldu + r0 + wc);
-      *reinterpret_cast<uint4*>(&tr[wr][wc]) = pk;
+      const int j = threadIdx.x & 7;
+      const uint4 pk = *reinterpret_cast<const uint4*>(u + static_cast<int64_t>(c0 + wr) * ldu + r0 + 8 * j);
+      *reinterpret_cast<uint4*>(&tr[wr][8 * (j ^ ((wr >> 3) & 7))]) = pk;
     }
     __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 8; ++q) tch[q] = *reinterpret_cast<const uint2*>(&tr[8 * tx + q][4 * (ty ^ (2 * (tx & 7)))]);
   }
   const float decay = a.decay, step = a.step;
   // column scales: the same 8 for all four rows of this thread
@@ -351,15 +370,17 @@ __global__ __launch_bounds__(256) void k_update(UpdateArgs a) {
   }
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const int lr = ty + 16 * k;
-    const int row = r0 + lr;
+    const int row = r0 + (tall ? 4 * ty + k : ty + 16 * k);
     if (row >= m || col >= n) continue;
     float uu[8];
     if (!tall) {
       load8<true>(u, static_cast<int64_t>(row) * ldu + col, uu);
     } else {
 #pragma unroll
-      for (int q = 0; q < 8; ++q) uu[q] = bf16_to_f32(tr[8 * tx + q][lr]);
+      for (int q = 0; q < 8; ++q) {
+        const uint32_t w = (k < 2) ? tch[q].x : tch[q].y;
+        uu[q] = bf16_to_f32(static_cast<uint16_t>((k & 1) ? (w >> 16) : (w & 0xffffu)));
+      }
     }
     float s[8];
     if (dir == 0) {
