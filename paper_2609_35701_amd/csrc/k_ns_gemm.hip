@@ -82,18 +82,20 @@ __device__ __forceinline__ int stage_byte(int rr, int c) {
 }
 
 // Scheduling pattern of one 16-MFMA k step: kReads LDS reads (for the next step) and
-// kDma LDS-bound buffer loads interleaved between the MFMAs.
+// kDma LDS-bound buffer loads interleaved between the MFMAs, the loads at most one per
+// two MFMAs (a load can hold up the wave's issue behind outstanding misses).
 template <int kReads, int kDma>
 __device__ __forceinline__ void sched_step() {
 #ifndef MEQ_NO_SCHED
 #define MEQ_SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
-#define MEQ_QUAD(r, d)          \
-  if (r > 0) MEQ_SG(0x100, r);  \
-  MEQ_SG(0x008, 1);             \
-  if (d > 0) MEQ_SG(0x020, d);  \
-  MEQ_SG(0x008, 1);             \
-  if (r > 0) MEQ_SG(0x100, r);  \
-  MEQ_SG(0x008, 1);             \
+#define MEQ_QUAD(r, d)                    \
+  if (r > 0) MEQ_SG(0x100, r);            \
+  MEQ_SG(0x008, 1);                       \
+  if (d > 0) MEQ_SG(0x020, (d + 1) / 2);  \
+  MEQ_SG(0x008, 1);                       \
+  if (r > 0) MEQ_SG(0x100, r);            \
+  MEQ_SG(0x008, 1);                       \
+  if (d > 1) MEQ_SG(0x020, d / 2);        \
   MEQ_SG(0x008, 1);
   constexpr int r0 = kReads / 8, r1 = kReads / 4 - kReads / 8;  // 4 (r0 + r1) reads
   constexpr int d = kDma / 4;
