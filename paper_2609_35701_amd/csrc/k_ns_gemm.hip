@@ -12,8 +12,9 @@
 // K advances in slabs through an LDS ring.  The Gram and polynomial products use slabs of
 // 32 k in a 4-stage ring (three slabs in flight while one is consumed, which covers the
 // latency of the loads that miss L2 over their long K); the apply product uses slabs of
-// 64 k in a 2-stage ring (half the barriers, whole 128-byte rows of its NT operand per
-// fetch), which measures faster for it and slower for the Gram product.  Global ->
+// 64 k (half the barriers, whole 128-byte rows of its NT operand per fetch), with operand
+// A (P) in 2 stages and operand B (X) in 3, so X is fetched a slab further ahead: all of
+// the 160 KiB of LDS.  Each choice measured faster than the alternatives.  Global ->
 // LDS traffic uses buffer loads that write LDS directly (no registers, no LDS store
 // instructions); 16-byte chunks are XOR-swizzled so fragment reads are free of bank
 // conflicts.  The epilogue stages the output tile (and, for P, the A tile it adds) in
@@ -113,29 +114,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // Ring geometry: the apply product takes the wide slabs.
   constexpr bool kWide = kNN;
   constexpr int BK = kWide ? 64 : 32;                 // k per slab
-  constexpr int kStages = kWide ? 2 : 4;
-  constexpr int kStageBytes = kWide ? 65536 : 32768;  // operand A slab + operand B slab
-  constexpr int kOpBytes = kStageBytes / 2;
+  constexpr int kStages = kWide ? 2 : 4;              // operand A stages (operand B: 3 for wide)
+  constexpr int kStageBytes = 32768;                  // narrow: A + B slab; wide: one operand's slab
+  constexpr int kOpBytes = 16384;                     // narrow: operand B within a stage
   constexpr int kRowBytes = 2 * BK;                   // one NT slab row
   constexpr int kDma = kWide ? 16 : 8;                // LDS-bound buffer loads per wave per slab
   // Ring stages as separate objects, so the compiler can tell the stage being read from
-  // the stages being filled (the 2-stage ring leaves st2_ and st3_ unreferenced).
+  // the stages being filled.  Narrow ring: st0..st3 are its 4 stages (st4_ unreferenced).
+  // Wide ring: st0, st1 hold operand A, st2, st3, st4 operand B; the epilogue stages its
+  // output in st0..st3 and the fused column sums in st4.
   __shared__ __attribute__((aligned(1024))) uint8_t st0_[kStageBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t st1_[kStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t st2_[kWide ? 16 : kStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t st3_[kWide ? 16 : kStageBytes];
-  __shared__ float colsum_[kNN ? 4 : 1][256];  // apply: per-wave column partials of the fused sums
+  __shared__ __attribute__((aligned(1024))) uint8_t st2_[kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st3_[kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st4_[kWide ? kStageBytes : 16];
   lds_u8* const st0 = (lds_u8*)st0_;
   lds_u8* const st1 = (lds_u8*)st1_;
   lds_u8* const st2 = (lds_u8*)st2_;
   lds_u8* const st3 = (lds_u8*)st3_;
+  lds_u8* const st4 = (lds_u8*)st4_;
+  // apply: per-wave column partials of the fused sums, in the ring's fifth buffer
+  typedef __attribute__((address_space(3))) float lds_f32;
+  lds_f32* const colsum = (lds_f32*)st4_;
   // The epilogue stages 64-row quarters of the output tile, 32 KiB each.
-  auto stage_of = [&](int q) {
-    if constexpr (kWide)
-      return q == 0 ? st0 : q == 1 ? st0 + 32768 : q == 2 ? st1 : st1 + 32768;
-    else
-      return q == 0 ? st0 : q == 1 ? st1 : q == 2 ? st2 : st3;
-  };
+  auto stage_of = [&](int q) { return q == 0 ? st0 : q == 1 ? st1 : q == 2 ? st2 : st3; };
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -198,35 +200,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * (nn_r & 3))));
   const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * ((2 + nn_r) & 3))));
 
-  auto issue_half_a = [&](lds_u8* buf, int kt) {
+  auto issue_half_a = [&](lds_u8* abuf, int kt) {
     const int k0 = kt * BK;
 #pragma unroll
     for (int i = 0; i < kDma / 2; ++i) {
       const int I = (kDma / 2) * wave + i;
-      dma16(rA, buf + I * 1024, (kWide && (i & 1)) ? vA_odd : vA, 2 * (kRowsPerDma * I * lda + k0));
+      dma16(rA, abuf + I * 1024, (kWide && (i & 1)) ? vA_odd : vA, 2 * (kRowsPerDma * I * lda + k0));
     }
   };
-  auto issue_half_b = [&](lds_u8* buf, int kt) {
+  auto issue_half_b = [&](lds_u8* bbuf, int kt) {
     const int k0 = kt * BK;
 #pragma unroll
     for (int i = 0; i < kDma / 2; ++i) {
       const int I = (kDma / 2) * wave + i;
       if (kNN)
-        dma16(rB, buf + kOpBytes + I * 1024, (i & 1) ? vB_nn1 : vB_nn0, 2 * ((k0 + 2 * I) * ldb));
+        dma16(rB, bbuf + I * 1024, (i & 1) ? vB_nn1 : vB_nn0, 2 * ((k0 + 2 * I) * ldb));
       else
-        dma16(rB, buf + kOpBytes + I * 1024, vB_nt, 2 * (kRowsPerDma * I * ldb + k0));
+        dma16(rB, bbuf + I * 1024, vB_nt, 2 * (kRowsPerDma * I * ldb + k0));
     }
   };
-  auto issue_slab = [&](lds_u8* buf, int kt) {
+  auto issue_slab = [&](lds_u8* buf, int kt) {  // narrow ring: both operands into one stage
     issue_half_a(buf, kt);
-    issue_half_b(buf, kt);
+    issue_half_b(buf + kOpBytes, kt);
   };
 
   // ---- fragment addresses (bytes within a stage)
   // NT fragment: row R = base + 32 i + lane%32 (base a multiple of 32), k chunk 2 kk + lane/32,
   // at slot chunk ^ swz(R), swz(R) = ((lane & 31) >> 2) & 3 (64-byte rows) or ((lane & 31) >> 1) & 7.
   const int offA = (wm * 128 + (lane & 31)) * kRowBytes;
-  const int offB_nt = kOpBytes + (wn * 128 + (lane & 31)) * kRowBytes;
+  const int offB_nt = (wn * 128 + (lane & 31)) * kRowBytes;
   const int nt_swz = kWide ? ((lane & 31) >> 1) & 7 : ((lane & 31) >> 2) & 3;
   int slot_kk[BK / 16];
 #pragma unroll
@@ -257,23 +259,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  auto load_frags = [&](const lds_u8* buf, int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[4]) {
+  auto load_frags = [&](const lds_u8* abuf, const lds_u8* bbuf, int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[4]) {
     const int oa = offA + slot_kk[kk];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(buf + oa + i * 32 * kRowBytes);
+    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(abuf + oa + i * 32 * kRowBytes);
     if (kNN) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const i16x4 lo =
-            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + (nn_off[j] + kOpBytes + 8192 * kk)));
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(bbuf + (nn_off[j] + 8192 * kk)));
         const i16x4 hi =
-            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(buf + (nn_off[j] + kOpBytes + 2048 + 8192 * kk)));
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(bbuf + (nn_off[j] + 2048 + 8192 * kk)));
         bfr[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
     } else {
       const int ob = offB_nt + slot_kk[kk];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const lds_bf16x8*>(buf + ob + j * 32 * kRowBytes);
+      for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const lds_bf16x8*>(bbuf + ob + j * 32 * kRowBytes);
     }
   };
 
@@ -290,17 +292,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
   };
 
-  // Software pipeline over slabs (slab s lives in ring stage s % kStages).  On entry to
-  // slab kt its first k step's fragments are already in registers (fa).  Each later step's
-  // fragments are read under the previous step's MFMAs.  Before the last step the wave waits
-  // for its own loads of slab kt + 1 and meets the other waves: slab kt + 1 has fully landed
-  // and no wave reads slab kt's stage any more, so the refill of that stage with slab
-  // kt + kStages starts (operand A) and slab kt + 1's first fragments are read under the last
-  // step's MFMAs.  Operand B of that refill goes out under the first step of slab kt + 1:
-  // split in two, the LDS-bound loads queue behind outstanding misses in smaller bursts,
-  // which keeps more of the MFMA stream moving (3% faster than one burst per slab).
+  // Software pipeline over slabs.  On entry to slab kt its first k step's fragments are
+  // already in registers (fa).  Each later step's fragments are read under the previous
+  // step's MFMAs.  Before the last step the wave waits for its own loads of slab kt + 1 and
+  // meets the other waves: slab kt + 1 has fully landed and no wave reads slab kt's stage
+  // any more, so that stage's refill starts (operand A) and slab kt + 1's first fragments
+  // are read under the last step's MFMAs.  Operand B goes out under the first step of the
+  // next slab: split in two, the LDS-bound loads queue behind outstanding misses in smaller
+  // bursts, which keeps more of the MFMA stream moving (3% faster than one burst per slab).
   // The waits count loads in issue order: at the barrier of slab kt everything issued after
-  // slab kt + 1's operand B may still be in flight, i.e. kStages - 2 slabs.
+  // slab kt + 1's last load may still be in flight.
   const int nk = g.K / BK;
   bf16x8 fa[4], fb[4], ga[4], gb[4];
   auto bar = [] {
@@ -311,41 +312,74 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     asm volatile("" ::: "memory");
   };
   constexpr int kReads = kNN ? 12 : 8;  // LDS read instructions per k step
-  // cur: slab kt's stage; nxt: slab kt + 1's; prv: the stage freed at the last barrier
+  // Narrow ring (slab s in stage s % 4).  cur: slab kt's stage; nxt: slab kt + 1's; prv: the
+  // stage freed at the last barrier, which receives operand B of slab kt + 3.
   auto slab = [&](lds_u8* cur, const lds_u8* nxt, lds_u8* prv, int kt) {
-    load_frags(cur, 1, ga, gb);
-    issue_half_b(prv, min(kt - 1 + kStages, nk - 1));  // second half of the slab started at the last barrier
+    load_frags(cur, cur + kOpBytes, 1, ga, gb);
+    issue_half_b(prv + kOpBytes, min(kt - 1 + kStages, nk - 1));  // second half of the slab started at the last barrier
     mfma16(fa, fb);
     sched_step<kReads, kDma / 2>();
-    if constexpr (kWide) {
-      load_frags(cur, 2, fa, fb);
-      mfma16(ga, gb);
-      sched_step<kReads, 0>();
-      load_frags(cur, 3, ga, gb);
-      mfma16(fa, fb);
-      sched_step<kReads, 0>();
-    }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave is done reading slab kt
     wait_vm<(kStages - 2) * kDma>();     // this wave's loads of slab kt + 1 have landed
     bar();
     issue_half_a(cur, min(kt + kStages, nk - 1));  // past the end: a harmless reload of the last slab
-    load_frags(nxt, 0, fa, fb);
+    load_frags(nxt, nxt + kOpBytes, 0, fa, fb);
+    mfma16(ga, gb);
+    sched_step<kReads, kDma / 2>();
+  };
+  // Wide ring.  Operand A of slab kt in ac (stage kt % 2), of kt + 1 in an; operand B of slab
+  // kt in bc (buffer kt % 3), of kt + 1 in bn, and bp (slab kt - 1's buffer, free since the
+  // last barrier) receives B of slab kt + 2 under the first step.  At the barrier only that
+  // operand B may still be in flight.
+  auto slab_w = [&](lds_u8* ac, const lds_u8* an, const lds_u8* bc, const lds_u8* bn, lds_u8* bp, int kt) {
+    load_frags(ac, bc, 1, ga, gb);
+    issue_half_b(bp, min(kt + 2, nk - 1));
+    mfma16(fa, fb);
+    sched_step<kReads, kDma / 2>();
+    load_frags(ac, bc, 2, fa, fb);
+    mfma16(ga, gb);
+    sched_step<kReads, 0>();
+    load_frags(ac, bc, 3, ga, gb);
+    mfma16(fa, fb);
+    sched_step<kReads, 0>();
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave is done reading slab kt
+    wait_vm<kDma / 2>();                 // all but operand B of slab kt + 2 have landed
+    bar();
+    issue_half_a(ac, min(kt + 2, nk - 1));  // past the end: a harmless reload of the last slab
+    load_frags(an, bn, 0, fa, fb);
     mfma16(ga, gb);
     sched_step<kReads, kDma / 2>();
   };
 
-  // ---- main loop: kStages slabs per trip so every stage is addressed statically.
-  // K is a multiple of 256 (zero padding), so the slab count is a multiple of 4.  The
-  // prologue issues all but operand B of slab kStages - 1, which the first slab sends.
+  // ---- main loop: every stage is addressed statically.  K is a multiple of 256 (zero
+  // padding), so the slab count is a multiple of 8 (narrow) or 4 (wide).  The wide ring's
+  // buffers repeat every 6 slabs (2 A stages, 3 B buffers), so its loop runs 6 slabs per
+  // trip and a tail of 2 or 4.
   if constexpr (kWide) {
-    issue_slab(st0, 0);
+    issue_half_a(st0, 0);
+    issue_half_b(st2, 0);
     issue_half_a(st1, 1);
-    wait_vm<kDma / 2>();
+    issue_half_b(st3, 1);
+    wait_vm<kDma>();
     bar();
-    load_frags(st0, 0, fa, fb);
-    for (int kt = 0; kt < nk; kt += 2) {
-      slab(st0, st1, st1, kt);
-      slab(st1, st0, st0, kt + 1);
+    load_frags(st0, st2, 0, fa, fb);
+    int kt = 0;
+    for (; kt + 6 <= nk; kt += 6) {
+      slab_w(st0, st1, st2, st3, st4, kt);
+      slab_w(st1, st0, st3, st4, st2, kt + 1);
+      slab_w(st0, st1, st4, st2, st3, kt + 2);
+      slab_w(st1, st0, st2, st3, st4, kt + 3);
+      slab_w(st0, st1, st3, st4, st2, kt + 4);
+      slab_w(st1, st0, st4, st2, st3, kt + 5);
+    }
+    if (kt + 2 <= nk) {
+      slab_w(st0, st1, st2, st3, st4, kt);
+      slab_w(st1, st0, st3, st4, st2, kt + 1);
+      kt += 2;
+    }
+    if (kt + 2 <= nk) {
+      slab_w(st0, st1, st4, st2, st3, kt);
+      slab_w(st1, st0, st2, st3, st4, kt + 1);
     }
   } else {
     issue_slab(st0, 0);
@@ -354,7 +388,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     issue_half_a(st3, 3);
     wait_vm<2 * kDma + kDma / 2>();
     bar();
-    load_frags(st0, 0, fa, fb);
+    load_frags(st0, st0 + kOpBytes, 0, fa, fb);
     for (int kt = 0; kt < nk; kt += 4) {
       slab(st0, st1, st3, kt);
       slab(st1, st2, st0, kt + 1);
@@ -477,9 +511,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       cs[3] = fmaf(x3, x3, cs[3]);
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) colsum_[wave][c4 + q] = cs[q];
+    for (int q = 0; q < 4; ++q) colsum[256 * wave + c4 + q] = cs[q];
     __syncthreads();
-    const float csum = (colsum_[0][t] + colsum_[1][t]) + (colsum_[2][t] + colsum_[3][t]);
+    const float csum = (colsum[t] + colsum[256 + t]) + (colsum[512 + t] + colsum[768 + t]);
     g.rpart[mat * g.stride_rpart + static_cast<int64_t>(tj) * (g.tiles_m * 256) + rowA0 + t] = rsum;
     g.cpart[mat * g.stride_cpart + static_cast<int64_t>(ti) * g.ldc + rowB0 + t] = csum;
   }
