@@ -9,12 +9,10 @@
 //
 // One workgroup = 4 waves = one 256 x 256 output tile; each wave owns a 128 x 128
 // quadrant as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation in AGPRs).
-// K advances in slabs through an LDS ring.  The Gram and polynomial products use slabs of
-// 32 k in a 4-stage ring (three slabs in flight while one is consumed, which covers the
-// latency of the loads that miss L2 over their long K); the apply product uses slabs of
-// 64 k (half the barriers, whole 128-byte rows of its NT operand per fetch), with operand
-// A (P) in 2 stages and operand B (X) in 3, so X is fetched a slab further ahead: all of
-// the 160 KiB of LDS.  Each choice measured faster than the alternatives.  Global ->
+// K advances in slabs of 64 through an LDS ring: operand A in 2 stages and operand B in 3
+// buffers of 32 KiB, so B is fetched a slab further ahead; that is all of the 160 KiB of
+// LDS.  This measured faster for all three products than a 4-stage ring of 32-wide slabs,
+// a 2-stage ring of 64-wide slabs, or 3 stages for operand A instead.  Global ->
 // LDS traffic uses buffer loads that write LDS directly (no registers, no LDS store
 // instructions); 16-byte chunks are XOR-swizzled so fragment reads are free of bank
 // conflicts.  The epilogue stages the output tile (and, for P, the A tile it adds) in
@@ -72,12 +70,11 @@ __device__ __forceinline__ void wait_vm() {
 }
 
 // LDS layouts (bytes).  Each 16-lane pass of an LDS access covers 256 bytes (64 banks).
-//   NT slab (256 rows x 32 k):   row r at r * 64; 16-byte chunk c (k = 8c..8c+7) at slot c ^ ((r >> 2) & 3),
+//   NT slab (256 rows x 64 k):   row r at r * 128; 16-byte chunk c (k = 8c..8c+7) at slot c ^ ((r >> 1) & 7),
 //                                so 16 consecutive rows read at one chunk fill the 256 bytes exactly.
-//   NT slab (256 rows x 64 k):   row r at r * 128; chunk c at slot c ^ ((r >> 1) & 7), same property.
-//   NN slab (BK k x 256 n):      row k at k * 512; chunk c (n = 8c..8c+7) at slot c ^ (4 (k & 3)), so the
+//   NN slab (64 k x 256 n):      row k at k * 512; chunk c (n = 8c..8c+7) at slot c ^ (4 (k & 3)), so the
 //                                4 rows x 4 chunks a 32-lane transpose read touches fill 256 bytes exactly.
-//   staged output (256 x 256):   row r in ring stage r / 64 at (r % 64) * 512; chunk c at slot c ^ (r & 31).
+//   staged output (256 x 256):   row r in ring buffer r / 64 at (r % 64) * 512; chunk c at slot c ^ (r & 31).
 __device__ __forceinline__ int stage_byte(int rr, int c) {
   return (rr & 63) * 512 + 16 * ((c >> 3) ^ (rr & 31)) + 2 * (c & 7);
 }
@@ -111,23 +108,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   constexpr bool kNN = kMode == 2;
   constexpr bool kSym = kMode != 2;
   constexpr bool kHasE = kMode == 1;
-  // Ring geometry: the apply product takes the wide slabs.
-  constexpr bool kWide = kNN;
-  constexpr int BK = kWide ? 64 : 32;                 // k per slab
-  constexpr int kStages = kWide ? 2 : 4;              // operand A stages (operand B: 3 for wide)
-  constexpr int kStageBytes = 32768;                  // narrow: A + B slab; wide: one operand's slab
-  constexpr int kOpBytes = 16384;                     // narrow: operand B within a stage
-  constexpr int kRowBytes = 2 * BK;                   // one NT slab row
-  constexpr int kDma = kWide ? 16 : 8;                // LDS-bound buffer loads per wave per slab
-  // Ring stages as separate objects, so the compiler can tell the stage being read from
-  // the stages being filled.  Narrow ring: st0..st3 are its 4 stages (st4_ unreferenced).
-  // Wide ring: st0, st1 hold operand A, st2, st3, st4 operand B; the epilogue stages its
-  // output in st0..st3 and the fused column sums in st4.
-  __shared__ __attribute__((aligned(1024))) uint8_t st0_[kStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t st1_[kStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t st2_[kStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t st3_[kStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t st4_[kWide ? kStageBytes : 16];
+  // Ring geometry
+  constexpr int BK = 64;               // k per slab
+  constexpr int kBufBytes = 32768;     // one operand's slab
+  constexpr int kRowBytes = 2 * BK;    // one NT slab row
+  constexpr int kDma = 16;             // LDS-bound buffer loads per wave per slab (8 per operand)
+  // Ring buffers as separate objects, so the compiler can tell the buffer being read from
+  // the buffers being filled: st0, st1 hold operand A, st2, st3, st4 operand B.  The
+  // epilogue stages its output in st0..st3 and the fused column sums in st4.
+  __shared__ __attribute__((aligned(1024))) uint8_t st0_[kBufBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st1_[kBufBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st2_[kBufBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st3_[kBufBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t st4_[kBufBytes];
   lds_u8* const st0 = (lds_u8*)st0_;
   lds_u8* const st1 = (lds_u8*)st1_;
   lds_u8* const st2 = (lds_u8*)st2_;
@@ -184,18 +177,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int rowA0 = ti * 256;
   const int rowB0 = tj * 256;  // NT: operand-B rows; NN: output columns
 
-  // ---- global -> LDS slab loads: kDma / 2 instructions per wave per operand (1 KiB each).
-  // NT: instruction I = (kDma / 2) wave + i covers R = 1024 / kRowBytes rows RI .. RI + R - 1;
-  //     lane -> row RI + lane / (64 / R), slot lane % (64 / R).  The slot holds chunk slot ^ swz:
-  //     64-byte rows:  swz = (row >> 2) & 3 = lane >> 4;
-  //     128-byte rows: swz = (row >> 1) & 7 = (lane >> 4) ^ 4 (I & 1).
+  // ---- global -> LDS slab loads: 8 instructions per wave per operand (1 KiB each).
+  // NT: instruction I = 8 wave + i covers rows 8I .. 8I + 7; lane -> row 8I + lane / 8,
+  //     slot lane % 8, which holds chunk slot ^ ((row >> 1) & 7) = slot ^ (lane >> 4) ^ 4 (I & 1).
   constexpr int kRowsPerDma = 1024 / kRowBytes;
-  const int nt_r = lane / (kRowBytes / 16);
-  const int nt_c = (lane % (kRowBytes / 16)) ^ (lane >> 4);
-  const int vA = 2 * ((rowA0 + nt_r) * lda + 8 * nt_c);
-  const int vA_odd = 2 * ((rowA0 + nt_r) * lda + 8 * (nt_c ^ 4));  // 128-byte rows, odd I
-  const int vB_nt = 2 * ((rowB0 + nt_r) * ldb + 8 * nt_c);         // 64-byte rows only
-  // NN: instruction I = (kDma / 2) wave + i covers k rows 2I, 2I + 1; lane -> row 2I + lane/32, slot lane%32.
+  const int nt_r = lane >> 3;
+  const int nt_c = (lane & 7) ^ (lane >> 4);
+  const int vA = 2 * ((rowA0 + nt_r) * lda + 8 * nt_c);                // even I
+  const int vA_odd = 2 * ((rowA0 + nt_r) * lda + 8 * (nt_c ^ 4));      // odd I
+  const int vB_nt = 2 * ((rowB0 + nt_r) * ldb + 8 * nt_c);
+  const int vB_nt_odd = 2 * ((rowB0 + nt_r) * ldb + 8 * (nt_c ^ 4));
+  // NN: instruction I = 8 wave + i covers k rows 2I, 2I + 1; lane -> row 2I + lane/32, slot lane%32.
   const int nn_r = lane >> 5;
   const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * (nn_r & 3))));
   const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * ((2 + nn_r) & 3))));
@@ -205,7 +197,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
     for (int i = 0; i < kDma / 2; ++i) {
       const int I = (kDma / 2) * wave + i;
-      dma16(rA, abuf + I * 1024, (kWide && (i & 1)) ? vA_odd : vA, 2 * (kRowsPerDma * I * lda + k0));
+      dma16(rA, abuf + I * 1024, (i & 1) ? vA_odd : vA, 2 * (kRowsPerDma * I * lda + k0));
     }
   };
   auto issue_half_b = [&](lds_u8* bbuf, int kt) {
@@ -216,20 +208,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       if (kNN)
         dma16(rB, bbuf + I * 1024, (i & 1) ? vB_nn1 : vB_nn0, 2 * ((k0 + 2 * I) * ldb));
       else
-        dma16(rB, bbuf + I * 1024, vB_nt, 2 * (kRowsPerDma * I * ldb + k0));
+        dma16(rB, bbuf + I * 1024, (i & 1) ? vB_nt_odd : vB_nt, 2 * (kRowsPerDma * I * ldb + k0));
     }
   };
-  auto issue_slab = [&](lds_u8* buf, int kt) {  // narrow ring: both operands into one stage
-    issue_half_a(buf, kt);
-    issue_half_b(buf + kOpBytes, kt);
-  };
 
-  // ---- fragment addresses (bytes within a stage)
+  // ---- fragment addresses (bytes within a buffer)
   // NT fragment: row R = base + 32 i + lane%32 (base a multiple of 32), k chunk 2 kk + lane/32,
-  // at slot chunk ^ swz(R), swz(R) = ((lane & 31) >> 2) & 3 (64-byte rows) or ((lane & 31) >> 1) & 7.
+  // at slot chunk ^ ((R >> 1) & 7) = chunk ^ (((lane & 31) >> 1) & 7).
   const int offA = (wm * 128 + (lane & 31)) * kRowBytes;
   const int offB_nt = (wn * 128 + (lane & 31)) * kRowBytes;
-  const int nt_swz = kWide ? ((lane & 31) >> 1) & 7 : ((lane & 31) >> 2) & 3;
+  const int nt_swz = ((lane & 31) >> 1) & 7;
   int slot_kk[BK / 16];
 #pragma unroll
   for (int kk = 0; kk < BK / 16; ++kk) slot_kk[kk] = 16 * ((2 * kk + h) ^ nt_swz);
@@ -292,16 +280,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
   };
 
-  // Software pipeline over slabs.  On entry to slab kt its first k step's fragments are
-  // already in registers (fa).  Each later step's fragments are read under the previous
-  // step's MFMAs.  Before the last step the wave waits for its own loads of slab kt + 1 and
-  // meets the other waves: slab kt + 1 has fully landed and no wave reads slab kt's stage
-  // any more, so that stage's refill starts (operand A) and slab kt + 1's first fragments
-  // are read under the last step's MFMAs.  Operand B goes out under the first step of the
-  // next slab: split in two, the LDS-bound loads queue behind outstanding misses in smaller
-  // bursts, which keeps more of the MFMA stream moving (3% faster than one burst per slab).
-  // The waits count loads in issue order: at the barrier of slab kt everything issued after
-  // slab kt + 1's last load may still be in flight.
+  // Software pipeline over slabs.  Operand A of slab s lives in buffer s % 2 of (st0, st1),
+  // operand B in buffer s % 3 of (st2, st3, st4).  On entry to slab kt its first k step's
+  // fragments are already in registers (fa).  Each later step's fragments are read under
+  // the previous step's MFMAs.  Under the first step, operand B of slab kt + 2 goes out into
+  // the B buffer that slab kt - 1 used (free since the last barrier).  Before the last step
+  // the wave waits for its own loads of slab kt + 1 (only that newest operand B may still be
+  // in flight: the waits count loads in issue order) and meets the other waves: slab kt + 1
+  // has fully landed and no wave reads slab kt's buffers any more, so operand A of slab
+  // kt + 2 goes into slab kt's A buffer, and slab kt + 1's first fragments are read, under
+  // the last step's MFMAs.  The two halves of a slab's loads thus go out one k step apart
+  // (one burst per slab measured 3% slower: the LDS-bound loads queue behind outstanding
+  // misses and hold up the MFMA stream), and operand B a slab earlier than operand A.
   const int nk = g.K / BK;
   bf16x8 fa[4], fb[4], ga[4], gb[4];
   auto bar = [] {
@@ -312,28 +302,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     asm volatile("" ::: "memory");
   };
   constexpr int kReads = kNN ? 12 : 8;  // LDS read instructions per k step
-  // Narrow ring (slab s in stage s % 4).  cur: slab kt's stage; nxt: slab kt + 1's; prv: the
-  // stage freed at the last barrier, which receives operand B of slab kt + 3.
-  auto slab = [&](lds_u8* cur, const lds_u8* nxt, lds_u8* prv, int kt) {
-    load_frags(cur, cur + kOpBytes, 1, ga, gb);
-    issue_half_b(prv + kOpBytes, min(kt - 1 + kStages, nk - 1));  // second half of the slab started at the last barrier
-    mfma16(fa, fb);
-    sched_step<kReads, kDma / 2>();
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave is done reading slab kt
-    wait_vm<(kStages - 2) * kDma>();     // this wave's loads of slab kt + 1 have landed
-    bar();
-    issue_half_a(cur, min(kt + kStages, nk - 1));  // past the end: a harmless reload of the last slab
-    load_frags(nxt, nxt + kOpBytes, 0, fa, fb);
-    mfma16(ga, gb);
-    sched_step<kReads, kDma / 2>();
-  };
-  // Wide ring.  Operand A of slab kt in ac (stage kt % 2), of kt + 1 in an; operand B of slab
-  // kt in bc (buffer kt % 3), of kt + 1 in bn, and bp (slab kt - 1's buffer, free since the
-  // last barrier) receives B of slab kt + 2 under the first step.  At the barrier only that
-  // operand B may still be in flight.
-  auto slab_w = [&](lds_u8* ac, const lds_u8* an, const lds_u8* bc, const lds_u8* bn, lds_u8* bp, int kt) {
+  // ac, an: A buffers of slabs kt, kt + 1; bc, bn: B buffers of slabs kt, kt + 1; bp: the
+  // B buffer of slab kt - 1, which receives slab kt + 2.
+  auto slab = [&](lds_u8* ac, const lds_u8* an, const lds_u8* bc, const lds_u8* bn, lds_u8* bp, int kt) {
     load_frags(ac, bc, 1, ga, gb);
-    issue_half_b(bp, min(kt + 2, nk - 1));
+    issue_half_b(bp, min(kt + 2, nk - 1));  // past the end: a harmless reload of the last slab
     mfma16(fa, fb);
     sched_step<kReads, kDma / 2>();
     load_frags(ac, bc, 2, fa, fb);
@@ -345,56 +318,39 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave is done reading slab kt
     wait_vm<kDma / 2>();                 // all but operand B of slab kt + 2 have landed
     bar();
-    issue_half_a(ac, min(kt + 2, nk - 1));  // past the end: a harmless reload of the last slab
+    issue_half_a(ac, min(kt + 2, nk - 1));
     load_frags(an, bn, 0, fa, fb);
     mfma16(ga, gb);
     sched_step<kReads, kDma / 2>();
   };
 
-  // ---- main loop: every stage is addressed statically.  K is a multiple of 256 (zero
-  // padding), so the slab count is a multiple of 8 (narrow) or 4 (wide).  The wide ring's
-  // buffers repeat every 6 slabs (2 A stages, 3 B buffers), so its loop runs 6 slabs per
-  // trip and a tail of 2 or 4.
-  if constexpr (kWide) {
-    issue_half_a(st0, 0);
-    issue_half_b(st2, 0);
-    issue_half_a(st1, 1);
-    issue_half_b(st3, 1);
-    wait_vm<kDma>();
-    bar();
-    load_frags(st0, st2, 0, fa, fb);
-    int kt = 0;
-    for (; kt + 6 <= nk; kt += 6) {
-      slab_w(st0, st1, st2, st3, st4, kt);
-      slab_w(st1, st0, st3, st4, st2, kt + 1);
-      slab_w(st0, st1, st4, st2, st3, kt + 2);
-      slab_w(st1, st0, st2, st3, st4, kt + 3);
-      slab_w(st0, st1, st3, st4, st2, kt + 4);
-      slab_w(st1, st0, st4, st2, st3, kt + 5);
-    }
-    if (kt + 2 <= nk) {
-      slab_w(st0, st1, st2, st3, st4, kt);
-      slab_w(st1, st0, st3, st4, st2, kt + 1);
-      kt += 2;
-    }
-    if (kt + 2 <= nk) {
-      slab_w(st0, st1, st4, st2, st3, kt);
-      slab_w(st1, st0, st2, st3, st4, kt + 1);
-    }
-  } else {
-    issue_slab(st0, 0);
-    issue_slab(st1, 1);
-    issue_slab(st2, 2);
-    issue_half_a(st3, 3);
-    wait_vm<2 * kDma + kDma / 2>();
-    bar();
-    load_frags(st0, st0 + kOpBytes, 0, fa, fb);
-    for (int kt = 0; kt < nk; kt += 4) {
-      slab(st0, st1, st3, kt);
-      slab(st1, st2, st0, kt + 1);
-      slab(st2, st3, st1, kt + 2);
-      slab(st3, st0, st2, kt + 3);
-    }
+  // ---- main loop: every buffer is addressed statically.  The buffers repeat every 6 slabs
+  // (2 A, 3 B), so the loop runs 6 slabs per trip; K is a multiple of 256 (zero padding),
+  // so the slab count is a multiple of 4 and the tail is 0, 2 or 4 slabs.
+  issue_half_a(st0, 0);
+  issue_half_b(st2, 0);
+  issue_half_a(st1, 1);
+  issue_half_b(st3, 1);
+  wait_vm<kDma>();  // slab 0 has landed
+  bar();
+  load_frags(st0, st2, 0, fa, fb);
+  int kt = 0;
+  for (; kt + 6 <= nk; kt += 6) {
+    slab(st0, st1, st2, st3, st4, kt);
+    slab(st1, st0, st3, st4, st2, kt + 1);
+    slab(st0, st1, st4, st2, st3, kt + 2);
+    slab(st1, st0, st2, st3, st4, kt + 3);
+    slab(st0, st1, st3, st4, st2, kt + 4);
+    slab(st1, st0, st4, st2, st3, kt + 5);
+  }
+  if (kt + 2 <= nk) {
+    slab(st0, st1, st2, st3, st4, kt);
+    slab(st1, st0, st3, st4, st2, kt + 1);
+    kt += 2;
+  }
+  if (kt + 2 <= nk) {
+    slab(st0, st1, st4, st2, st3, kt);
+    slab(st1, st0, st2, st3, st4, kt + 1);
   }
   wait_vm<0>();
   __syncthreads();
@@ -402,7 +358,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // ---- epilogue.  OUT is the 256 x 256 tile written with whole-row stores:
   //   apply:     OUT = C(ti, tj); lane holds OUT[128 wm + 32 i + lane%32][128 wn + 32 j + 8 (v/4) + 4 (lane/32) + v%4]
   //   Gram/poly: OUT = C(tj, ti) = C(ti, tj)^T; lane holds OUT[128 wn + 32 j + lane%32][128 wm + 32 i + ...]
-  // OUT row r is staged in ring stage r / 64.
+  // OUT row r is staged in ring buffer r / 64 (st0..st3).
   const int out_row0 = kNN ? rowA0 : rowB0;
   const int out_col0 = kNN ? rowB0 : rowA0;
   float s = 1.f;
