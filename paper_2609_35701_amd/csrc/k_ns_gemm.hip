@@ -389,36 +389,53 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     __syncthreads();
   }
 
-  // combine: each lane owns 4 consecutive OUT columns per (i, j, v/4).  All staged E reads
-  // come before any staged write so that they can all be in flight at once.
+  // combine: each lane owns 4 consecutive OUT columns per (i, j, v/4).  Block by block
+  // (fenced against the scheduler, which otherwise hoists every product at once and runs out
+  // of registers), with the staged E values of the next block read while this one is
+  // computed.  All staged E reads come before any staged write.
   u32x2 packed[4][4][4];
+  auto e_read = [&](int i, int j, u32x2 (&e)[4]) {
+    const int r = 128 * own_row + 32 * (kNN ? i : j) + (lane & 31);
+    const lds_u8* src = stage_of(2 * own_row + ((kNN ? i : j) >> 1));
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+    for (int vq = 0; vq < 4; ++vq) {
+      const int c = 128 * own_col + 32 * (kNN ? j : i) + 8 * vq + 4 * h;
+      e[vq] = *reinterpret_cast<const lds_u32x2*>(src + stage_byte(r, c));
+    }
+  };
+  u32x2 ecur[4], enext[4];
+  if (kHasE) e_read(0, 0, ecur);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = 128 * own_row + 32 * (kNN ? i : j) + (lane & 31);
-      const lds_u8* src = stage_of(2 * own_row + ((kNN ? i : j) >> 1));
+  for (int b = 0; b < 16; ++b) {
+    const int i = b >> 2, j = b & 3;
+    if (kHasE && b < 15) e_read((b + 1) >> 2, (b + 1) & 3, enext);
+    if (kHasE) __builtin_amdgcn_sched_barrier(0);
+    const int r = 128 * own_row + 32 * (kNN ? i : j) + (lane & 31);
 #pragma unroll
-      for (int vq = 0; vq < 4; ++vq) {
-        const int c = 128 * own_col + 32 * (kNN ? j : i) + 8 * vq + 4 * h;
-        float o[4];
+    for (int vq = 0; vq < 4; ++vq) {
+      const int c = 128 * own_col + 32 * (kNN ? j : i) + 8 * vq + 4 * h;
+      float o[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = aa * acc[i][j][4 * vq + q];
-        if (kHasE) {
-          const u32x2 e = *reinterpret_cast<const lds_u32x2*>(src + stage_byte(r, c));
-          o[0] = fmaf(ae, bf16_to_f32(e.x & 0xffffu), o[0]);
-          o[1] = fmaf(ae, bf16_to_f32(e.x >> 16), o[1]);
-          o[2] = fmaf(ae, bf16_to_f32(e.y & 0xffffu), o[2]);
-          o[3] = fmaf(ae, bf16_to_f32(e.y >> 16), o[3]);
-        }
-        if (kSym) {
-          // OUT is symmetric here, so OUT[r][c + q] is on the diagonal when r == c + q
-#pragma unroll
-          for (int q = 0; q < 4; ++q) o[q] += (r == c + q) ? ad : 0.f;
-        }
-        packed[i][j][vq].x = pack_bf16x2(o[0], o[1]);
-        packed[i][j][vq].y = pack_bf16x2(o[2], o[3]);
+      for (int q = 0; q < 4; ++q) o[q] = aa * acc[i][j][4 * vq + q];
+      if (kHasE) {
+        const u32x2 e = ecur[vq];
+        o[0] = fmaf(ae, bf16_to_f32(e.x & 0xffffu), o[0]);
+        o[1] = fmaf(ae, bf16_to_f32(e.x >> 16), o[1]);
+        o[2] = fmaf(ae, bf16_to_f32(e.y & 0xffffu), o[2]);
+        o[3] = fmaf(ae, bf16_to_f32(e.y >> 16), o[3]);
       }
+      if (kSym) {
+        // OUT is symmetric here, so OUT[r][c + q] is on the diagonal when r == c + q
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] += (r == c + q) ? ad : 0.f;
+      }
+      packed[i][j][vq].x = pack_bf16x2(o[0], o[1]);
+      packed[i][j][vq].y = pack_bf16x2(o[2], o[3]);
+    }
+    if (kHasE) {
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int vq = 0; vq < 4; ++vq) ecur[vq] = enext[vq];
     }
   }
 #pragma unroll
