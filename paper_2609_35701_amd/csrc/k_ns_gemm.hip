@@ -9,10 +9,10 @@
 //
 // One workgroup = 4 waves = one 256 x 256 output tile; each wave owns a 128 x 128
 // quadrant as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation in AGPRs).
-// K advances in slabs of 64 through an LDS ring: operand A in 2 stages and operand B in 3
+// K advances in slabs of 64 through an LDS ring: operand A in 2 buffers and operand B in 3
 // buffers of 32 KiB, so B is fetched a slab further ahead; that is all of the 160 KiB of
 // LDS.  This measured faster for all three products than a 4-stage ring of 32-wide slabs,
-// a 2-stage ring of 64-wide slabs, or 3 stages for operand A instead.  Global ->
+// a 2-stage ring of 64-wide slabs, or 3 buffers for operand A instead.  Global ->
 // LDS traffic uses buffer loads that write LDS directly (no registers, no LDS store
 // instructions); 16-byte chunks are XOR-swizzled so fragment reads are free of bank
 // conflicts.  The epilogue stages the output tile (and, for P, the A tile it adds) in
@@ -192,18 +192,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * (nn_r & 3))));
   const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * ((2 + nn_r) & 3))));
 
-  auto issue_half_a = [&](lds_u8* abuf, int kt) {
+  auto issue_half_a = [&](lds_u8* abuf, int kt, int i0 = 0, int i1 = kDma / 2) {
     const int k0 = kt * BK;
 #pragma unroll
-    for (int i = 0; i < kDma / 2; ++i) {
+    for (int i = i0; i < i1; ++i) {
       const int I = (kDma / 2) * wave + i;
       dma16(rA, abuf + I * 1024, (i & 1) ? vA_odd : vA, 2 * (kRowsPerDma * I * lda + k0));
     }
   };
-  auto issue_half_b = [&](lds_u8* bbuf, int kt) {
+  auto issue_half_b = [&](lds_u8* bbuf, int kt, int i0 = 0, int i1 = kDma / 2) {
     const int k0 = kt * BK;
 #pragma unroll
-    for (int i = 0; i < kDma / 2; ++i) {
+    for (int i = i0; i < i1; ++i) {
       const int I = (kDma / 2) * wave + i;
       if (kNN)
         dma16(rB, bbuf + I * 1024, (i & 1) ? vB_nn1 : vB_nn0, 2 * ((k0 + 2 * I) * ldb));
@@ -282,16 +282,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
   // Software pipeline over slabs.  Operand A of slab s lives in buffer s % 2 of (st0, st1),
   // operand B in buffer s % 3 of (st2, st3, st4).  On entry to slab kt its first k step's
-  // fragments are already in registers (fa).  Each later step's fragments are read under
-  // the previous step's MFMAs.  Under the first step, operand B of slab kt + 2 goes out into
-  // the B buffer that slab kt - 1 used (free since the last barrier).  Before the last step
-  // the wave waits for its own loads of slab kt + 1 (only that newest operand B may still be
-  // in flight: the waits count loads in issue order) and meets the other waves: slab kt + 1
-  // has fully landed and no wave reads slab kt's buffers any more, so operand A of slab
-  // kt + 2 goes into slab kt's A buffer, and slab kt + 1's first fragments are read, under
-  // the last step's MFMAs.  The two halves of a slab's loads thus go out one k step apart
-  // (one burst per slab measured 3% slower: the LDS-bound loads queue behind outstanding
-  // misses and hold up the MFMA stream), and operand B a slab earlier than operand A.
+  // fragments are already in registers (fa).  Each later step's fragments are read under the
+  // previous step's MFMAs.  Before the last step the wave waits for its own loads of slab
+  // kt + 1 and meets the other waves: slab kt + 1 has fully landed and no wave reads slab
+  // kt's buffers any more; slab kt + 1's first fragments are then read under the last step's
+  // MFMAs.  Each k step also issues 4 of the 16 LDS-bound loads a slab needs per wave:
+  //   step 0: the second half of operand A of slab kt + 1 (its buffer was freed a step ago),
+  //   steps 1, 2: operand B of slab kt + 2, into the B buffer slab kt - 1 used,
+  //   step 3 (after the barrier): the first half of operand A of slab kt + 2, into slab kt's.
+  // At the barrier only operand B of slab kt + 2 may still be in flight (the waits count
+  // loads in issue order).  An LDS-bound load can hold up the wave's issue while misses are
+  // outstanding, so the loads go out evenly, at most one per 4 MFMAs (measured on the apply
+  // product: two bursts instead of one 3% faster, spaced within the step 2% more, four even
+  // parts another 2-3%); operand B's extra slab of lead time is what makes that possible.
   const int nk = g.K / BK;
   bf16x8 fa[4], fb[4], ga[4], gb[4];
   auto bar = [] {
@@ -303,25 +306,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   };
   constexpr int kReads = kNN ? 12 : 8;  // LDS read instructions per k step
   // ac, an: A buffers of slabs kt, kt + 1; bc, bn: B buffers of slabs kt, kt + 1; bp: the
-  // B buffer of slab kt - 1, which receives slab kt + 2.
-  auto slab = [&](lds_u8* ac, const lds_u8* an, const lds_u8* bc, const lds_u8* bn, lds_u8* bp, int kt) {
+  // B buffer of slab kt - 1, which receives slab kt + 2.  Past the end the loads are harmless
+  // reloads of the last slab.
+  auto slab = [&](lds_u8* ac, lds_u8* an, const lds_u8* bc, const lds_u8* bn, lds_u8* bp, int kt) {
     load_frags(ac, bc, 1, ga, gb);
-    issue_half_b(bp, min(kt + 2, nk - 1));  // past the end: a harmless reload of the last slab
+    issue_half_a(an, min(kt + 1, nk - 1), 4, 8);  // second half of A of slab kt + 1
     mfma16(fa, fb);
-    sched_step<kReads, kDma / 2>();
+    sched_step<kReads, 4>();
     load_frags(ac, bc, 2, fa, fb);
+    issue_half_b(bp, min(kt + 2, nk - 1), 0, 4);  // B of slab kt + 2, first half
     mfma16(ga, gb);
-    sched_step<kReads, 0>();
+    sched_step<kReads, 4>();
     load_frags(ac, bc, 3, ga, gb);
+    issue_half_b(bp, min(kt + 2, nk - 1), 4, 8);  // second half
     mfma16(fa, fb);
-    sched_step<kReads, 0>();
+    sched_step<kReads, 4>();
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave is done reading slab kt
     wait_vm<kDma / 2>();                 // all but operand B of slab kt + 2 have landed
     bar();
-    issue_half_a(ac, min(kt + 2, nk - 1));
+    issue_half_a(ac, min(kt + 2, nk - 1), 0, 4);  // first half of A of slab kt + 2
     load_frags(an, bn, 0, fa, fb);
     mfma16(ga, gb);
-    sched_step<kReads, kDma / 2>();
+    sched_step<kReads, 4>();
   };
 
   // ---- main loop: every buffer is addressed statically.  The buffers repeat every 6 slabs
@@ -329,9 +335,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // so the slab count is a multiple of 4 and the tail is 0, 2 or 4 slabs.
   issue_half_a(st0, 0);
   issue_half_b(st2, 0);
-  issue_half_a(st1, 1);
   issue_half_b(st3, 1);
-  wait_vm<kDma>();  // slab 0 has landed
+  issue_half_a(st1, 1, 0, 4);  // its second half goes out under slab 0's first step
+  wait_vm<12>();               // slab 0 has landed
   bar();
   load_frags(st0, st2, 0, fa, fb);
   int kt = 0;
