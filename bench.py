@@ -144,17 +144,26 @@ XCDS = 8
 
 
 def ns_launch_flops(wl) -> dict:
-    """Per launch of each NS product over all shape groups: (algorithmic symmetric-aware flops,
-    flops the 256 x 256 tiles execute, padding and the lower half of diagonal tiles included)."""
+    """Per step, for each NS kernel template over all shape groups: (algorithmic symmetric-aware
+    flops, flops the 256 x 256 tiles execute, padding and the lower half of diagonal tiles
+    included), under the default schedule of each shape group."""
+    from paper_2609_35701_amd import meq
+
+    plan = meq.Plan([(m.rows, m.cols) for m in wl.matrices], wl.param_dtype)
+    segs = {(s, l): plan.schedule(g) for g, (s, l, _) in enumerate(plan.groups())}
     out = {"k_ns_gemm<0>": [0, 0], "k_ns_gemm<1>": [0, 0], "k_ns_gemm<2>": [0, 0]}
     for m in wl.matrices:
         s, l = min(m.rows, m.cols), max(m.rows, m.cols)
         sp, lp = -(-s // 256) * 256, -(-l // 256) * 256
         tm, tl = sp // 256, lp // 256
         tri = tm * (tm + 1) // 2
-        for k, alg, exe in (("k_ns_gemm<0>", s * s * l, tri * 2 * 256 * 256 * lp),
-                            ("k_ns_gemm<1>", s ** 3, tri * 2 * 256 * 256 * sp),
-                            ("k_ns_gemm<2>", 2 * s * s * l, tm * tl * 2 * 256 * 256 * sp)):
+        sg = segs[(s, l)]
+        nseg, steps = len(sg), sum(sg)
+        nsprod = sum(3 * (j - 1) for j in sg)
+        for k, alg, exe in (("k_ns_gemm<0>", nseg * s * s * l + nsprod * s ** 3,
+                             nseg * tri * 2 * 256 * 256 * lp + nsprod * tri * 2 * 256 * 256 * sp),
+                            ("k_ns_gemm<1>", steps * s ** 3, steps * tri * 2 * 256 * 256 * sp),
+                            ("k_ns_gemm<2>", nseg * 2 * s * s * l, nseg * tm * tl * 2 * 256 * 256 * sp)):
             out[k][0] += alg
             out[k][1] += exe
     return out
@@ -195,12 +204,20 @@ def summarize_mfma(run_dir: str, out: str, command: str, workload: str, note: st
         f.write("".join(lines))
 
 
-def ns_flops(s: int, l: int, steps: int):
-    """Algorithmic Newton-Schulz flops of one matrix: (symmetric-aware total, apply-only, dense total)."""
-    sym = steps * (3 * s * s * l + s ** 3)
-    apply = steps * (2 * s * s * l)
-    dense = steps * (4 * s * s * l + 2 * s ** 3)
-    return sym, apply, dense
+def ns_flops(s: int, l: int, segs) -> dict:
+    """Algorithmic Newton-Schulz flops of one s x l matrix (wide orientation) under a schedule
+    of Gram-space segments (all ones: eq. "ns" as printed), symmetric products counted once:
+    per segment one X X^T (s^2 l) and one X product (2 s^2 l); per step one polynomial
+    product (s^3); per segment of j steps 3 (j - 1) products P A, P T, P Q (s^3 each).
+    "printed" is the printed iteration's symmetric-aware count K (3 s^2 l + s^3) and "dense"
+    its literal dense count K (4 s^2 l + 2 s^3), for any schedule."""
+    nseg, steps = len(segs), sum(segs)
+    out = {"gram": nseg * s * s * l, "poly": steps * s ** 3, "gram_space": sum(3 * (j - 1) for j in segs) * s ** 3,
+           "apply": nseg * 2 * s * s * l}
+    out["total"] = sum(out.values())
+    out["printed"] = steps * (3 * s * s * l + s ** 3)
+    out["dense"] = steps * (4 * s * s * l + 2 * s ** 3)
+    return out
 
 
 def stage_bytes(elems: int, param_bytes: int, rowcol_pass: bool):
@@ -253,7 +270,11 @@ def extras_leg(params, wl, lr: float, steps: int, warmup: int) -> dict:
     moon = meq.HiddenWeightUpdate(params, meq.default_hparams(update_rule=meq.RULE_MOONLIGHT))
     out["moonlight_hidden"] = time_steps(moon, g_hidden, lr, steps, warmup,
                                          [meq.K_ROWCOL, meq.K_SELECT, meq.K_UPDATE])
-    del moon, g_hidden
+    # the printed iteration everywhere (no Gram-space segments): what the segments save
+    literal = meq.HiddenWeightUpdate(params, meq.default_hparams(ns_gram_steps=1))
+    out["printed_iteration_hidden"] = time_steps(literal, g_hidden, lr, steps, warmup,
+                                                 [meq.K_GRAM, meq.K_POLY, meq.K_APPLY, meq.K_GRAM_SPACE])
+    del moon, literal, g_hidden
     torch.cuda.empty_cache()
     # remaining 2D parameters: the Llama token embedding and LM head (32000 x 2048, untied), bf16
     aux_p = [torch.randn(32000, 2048, device=dev).mul_(0.02).to(torch.bfloat16) for _ in range(2)]
@@ -480,25 +501,29 @@ def main() -> int:
     print(f"# bench: {ms_per_step:.3f} ms/step; " +
           ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in kern.items() if v["launches_per_step"]), file=sys.stderr, flush=True)
 
-    sym = apply = dense = 0
+    sched = {(gs, gl): upd.plan.schedule(g) for g, (gs, gl, _) in enumerate(upd.plan.groups())}
+    fl = {}
     for m in wl.matrices:
         s, l = min(m.rows, m.cols), max(m.rows, m.cols)
-        a, b, c = ns_flops(s, l, hp.ns_steps)
-        sym, apply, dense = sym + a, apply + b, dense + c
+        for k, v in ns_flops(s, l, sched[(s, l)]).items():
+            fl[k] = fl.get(k, 0) + v
     pbytes = 2 if wl.param_dtype == "bf16" else 4
     sb = stage_bytes(wl.elements, pbytes, kern["rowcol"]["launches_per_step"] > 0)
-    ns_ms = sum(kern[k]["ms_per_step"] for k in ("gram", "poly", "apply"))
+    ns_kinds = ("gram", "poly", "gram_space", "apply")
+    ns_ms = sum(kern[k]["ms_per_step"] for k in ns_kinds)
     ap_ms = kern["apply"]["ms_per_step"]
-    apply_tflops = apply / (ap_ms * 1e-3) / 1e12
-    roofline = {"bound": "mfma", "kernel": "k_ns_gemm<2> (X <- aX + P X, bf16 MFMA)",
+    apply_tflops = fl["apply"] / (ap_ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "kernel": "k_ns_gemm<2> (X <- P X, or Q X after a Gram-space segment; bf16 MFMA)",
                 "achieved": apply_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": apply_tflops / PEAK_BF16_TFLOPS, "traffic": recorded_traffic(wl.name),
-                "flops_per_launch": apply / max(kern["apply"]["launches_per_step"], 1),
+                "flops_per_launch": fl["apply"] / max(kern["apply"]["launches_per_step"], 1),
                 "avg_launch_ms": kern["apply"]["avg_launch_ms"]}
     stages = {
-        "ns_tflops_sym": sym / (ns_ms * 1e-3) / 1e12,
-        "ns_frac_of_peak_sym": sym / (ns_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-        "ns_tflops_dense": dense / (ns_ms * 1e-3) / 1e12,
+        "ns_tflops": fl["total"] / (ns_ms * 1e-3) / 1e12,
+        "ns_frac_of_peak": fl["total"] / (ns_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "ns_tflops_by_kernel": {k: fl[k] / (kern[k]["ms_per_step"] * 1e-3) / 1e12
+                                for k in ns_kinds if kern[k]["ms_per_step"] > 0},
+        "ns_printed_equiv_tflops": fl["printed"] / (ns_ms * 1e-3) / 1e12,
         "momentum_gbs": sb["momentum"] / (kern["momentum"]["ms_per_step"] * 1e-3) / 1e9,
         "update_gbs": sb["update"] / (kern["update"]["ms_per_step"] * 1e-3) / 1e9,
         "byte_stages_ms": sum(kern[k]["ms_per_step"] for k in sb),
@@ -522,8 +547,11 @@ def main() -> int:
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": wl.name, "matrices": wl.count, "elements": wl.elements,
                    "param_dtype": wl.param_dtype, "grad_dtype": wl.param_dtype, "momentum_dtype": "f32",
-                   "ns_steps": hp.ns_steps, "ns_tflop_per_step_sym": sym / 1e12,
-                   "ns_tflop_per_step_dense": dense / 1e12},
+                   "ns_steps": hp.ns_steps, "ns_gram_steps": hp.ns_gram_steps,
+                   "ns_schedules": {f"{k[0]}x{k[1]}": v for k, v in sched.items()},
+                   "ns_tflop_per_step": fl["total"] / 1e12,
+                   "ns_tflop_per_step_printed_sym": fl["printed"] / 1e12,
+                   "ns_tflop_per_step_printed_dense": fl["dense"] / 1e12},
         "roofline": roofline, "cpu_baseline": cpu, "stages": stages,
         "kernels_ms_per_step": {k: v["ms_per_step"] for k, v in kern.items() if v["launches_per_step"]},
         "extras": extras,

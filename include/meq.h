@@ -82,7 +82,24 @@ typedef enum { MEQ_RULE_MEQMUON = 0, MEQ_RULE_MOONLIGHT = 1 } meq_update_rule;
  *   nesterov       0: normalize B_t (Algorithm "MeqMuon");
  *                  1: normalize G_t + mu * B_t (the experiments' hidden weights)
  *   update_rule    meq_update_rule; MEQ_RULE_MOONLIGHT only for MEQ_PARAM_HIDDEN plans
- * ns_steps, ns_a/b/c only matter for hidden plans but are validated for every plan.
+ *   ns_gram_steps  g, 1 <= g <= 2: the most Newton-Schulz steps one Gram-space segment
+ *                  covers.  g = 1 runs eq. "ns" as printed: every step forms A = X X^T,
+ *                  the polynomial P = a I + b A + c A A and X <- P X.  With g = 2, a
+ *                  matrix whose padded long side is at least twice its padded short side
+ *                  runs its K steps in segments of at most 2 steps: a segment forms
+ *                  A = X X^T once, then iterates on s x s matrices only (each step's P is a
+ *                  polynomial of A, so A_{k+1} = P_k A_k P_k, and the segment's product
+ *                  Q = P_{k+1} P_k is symmetric), and ends with one product X <- Q X.
+ *                  Equal to eq. "ns" in exact arithmetic; it replaces most s x l products
+ *                  by s x s ones.  Segments are 2 steps long, the last one takes the
+ *                  remainder (K = 5: 2 + 2 + 1).  Default 2.  Longer segments are not
+ *                  offered: in bf16, A = X X^T squares the spread of the singular values and
+ *                  the segment's rounding errors are not corrected by later printed steps;
+ *                  3 + 2 reaches about 3% relative error in the Newton-Schulz output on
+ *                  small ill-conditioned inputs, at the 3e-2 bound that 2 + 2 + 1 meets with
+ *                  room to spare (about 1.3%, against about 0.9% for the printed iteration).
+ * ns_steps, ns_a/b/c and ns_gram_steps only matter for hidden plans but are validated for
+ * every plan.
  */
 typedef struct {
   float mu;
@@ -95,6 +112,7 @@ typedef struct {
   float zero_rms_delta;
   int32_t nesterov;
   int32_t update_rule;
+  int32_t ns_gram_steps;
 } meq_hparams;
 
 /*
@@ -118,7 +136,7 @@ typedef struct meq_plan meq_plan; /* opaque; owns host metadata only */
 
 /* Fill *hp with the paper's defaults: mu 0.95, rho 0.2, lambda 0.1, K 5,
  * (a, b, c) = (3.4445, -4.7750, 2.0315), delta 1e-7, nesterov 0,
- * update_rule MEQ_RULE_MEQMUON.  No-op on null. */
+ * update_rule MEQ_RULE_MEQMUON, ns_gram_steps 2.  No-op on null. */
 void meq_default_hparams(meq_hparams* hp);
 
 /*
@@ -202,14 +220,22 @@ int32_t meq_plan_num_groups(const meq_plan* plan);
  * wide orientation) and its number of matrices. */
 meq_status meq_plan_group(const meq_plan* plan, int32_t g, int64_t* s, int64_t* l, int32_t* count);
 
+/* Newton-Schulz schedule of shape group g: *nsegs receives the number of segments and
+ * segs[0 .. min(*nsegs, max_segs) - 1] their lengths in steps (they sum to ns_steps; all
+ * ones is the iteration of eq. "ns" as printed, see ns_gram_steps).  segs may be null
+ * when max_segs is 0. */
+meq_status meq_plan_group_schedule(const meq_plan* plan, int32_t g, int32_t* segs, int32_t max_segs,
+                                   int32_t* nsegs);
+
 /* Buffers of the workspace that tests may inspect after a step.
  * Hidden plans: all six.  Aux plans: MEQ_BUF_ROW_RMS (r of V), MEQ_BUF_COL_RMS
  * (c of N_r(V)).  Vector plans: MEQ_BUF_NORMSQ (||V||_2^2).  Other pairs are
  * MEQ_ERR_INVALID_ARG. */
 typedef enum {
   MEQ_BUF_X0 = 0,      /* bf16 V (not yet divided by ||V||_F), wide orientation s x l, ld = padded l;
-                          still intact after a step only when ns_steps == 1 (later Newton-Schulz
-                          steps reuse the buffer)                                                  */
+                          still intact after a step only when the matrix's Newton-Schulz schedule
+                          has one segment (meq_plan_group_schedule; later segments reuse the
+                          buffer)                                                                */
   MEQ_BUF_U = 1,       /* bf16 Newton-Schulz output U, wide orientation s x l, ld = padded l          */
   MEQ_BUF_NORMSQ = 2,  /* double ||V||_F^2, 1 x 1                                                    */
   MEQ_BUF_ROW_RMS = 3, /* double r of U in the matrix's own orientation, 1 x rows                      */
@@ -235,8 +261,8 @@ typedef enum {
   MEQ_K_MOMENTUM = 0, /* momentum + ||V||^2 partials + bf16 V in wide orientation            */
   MEQ_K_NORM = 1,     /* ||V||_F^2 finalization                                                */
   MEQ_K_GRAM = 2,     /* A = X X^T (symmetric tiles)                                           */
-  MEQ_K_POLY = 3,     /* P = b A + c A A (symmetric tiles)                                     */
-  MEQ_K_APPLY = 4,    /* X <- a X + P X                                                        */
+  MEQ_K_POLY = 3,     /* P = a I + b A + c A A (symmetric tiles)                               */
+  MEQ_K_APPLY = 4,    /* X <- P X, or X <- Q X at the end of a Gram-space segment              */
   MEQ_K_ROWCOL = 5,   /* row and column sums of squares of U                                    */
   MEQ_K_SELECT = 6,   /* CVs, direction, scale vector                                           */
   MEQ_K_UPDATE = 7,   /* decoupled weight decay + normalized update write-back                   */
@@ -244,7 +270,8 @@ typedef enum {
   MEQ_K_AUX_COLS = 9,   /* aux: column RMS of N_r(V) (partials + finalization)                   */
   MEQ_K_AUX_UPDATE = 10, /* aux: decoupled weight decay + two-sided normalized update            */
   MEQ_K_VECTOR = 11,    /* vector: momentum, global RMS and write-back in one kernel             */
-  MEQ_K_COUNT = 12
+  MEQ_K_GRAM_SPACE = 12, /* Gram-space segment products P A, P T, P Q (symmetric tiles)         */
+  MEQ_K_COUNT = 13
 } meq_kernel_kind;
 
 /* Bracket every launch of the kinds in `kind_mask` (bit k = meq_kernel_kind k)

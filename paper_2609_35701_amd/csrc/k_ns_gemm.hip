@@ -4,6 +4,8 @@
 //   X_{k+1} = P_k X_k              (NN: X_k is staged K-major and read with LDS transpose reads)
 // which is a X_k + (b A_k + c A_k A_k) X_k regrouped: the a X_k term rides on the
 // diagonal of P_k, so the apply epilogue reads nothing besides its accumulators.
+// A Gram-space segment uses the same three kernels: the symmetric NT product also forms
+// P_k A_k, P_k T and P_k Q (commuting symmetric factors), and the NN product X <- Q X.
 // X_0 = V / ||V||_F is folded in: the bf16 buffer holds V, the k = 0 Gram epilogue
 // scales by 1/||V||^2 and the k = 0 apply epilogue by 1/||V||.
 //
@@ -368,7 +370,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int out_row0 = kNN ? rowA0 : rowB0;
   const int out_col0 = kNN ? rowB0 : rowA0;
   float s = 1.f;
-  if (args.scale_kind != 0) s = g.fold[2 * mat + (args.scale_kind - 1)];
+  if (g.scale_kind != 0) s = g.fold[2 * mat + (g.scale_kind - 1)];
   const float ae = args.alpha_e * s, aa = args.alpha_acc * s;
   const float ad = (kSym && ti == tj) ? args.alpha_diag * s : 0.f;  // diagonal tiles only
   const int own_row = kNN ? wm : wn;  // 128-row half holding this wave's OUT rows
@@ -457,6 +459,50 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
     }
   __syncthreads();
+
+  if (kSym && ti == tj && g.symmetrize) {
+    // A product of two different commuting symmetric factors (P A, P T, P Q) is symmetric only
+    // up to rounding, and the next product reads the stored matrix as its own transpose.  The
+    // off-diagonal tiles store the upper block triangle of the product and its mirror; a
+    // diagonal tile keeps the same triangle (OUT[r][c] with r >= c, the product's upper
+    // triangle) and copies it onto the other half: OUT[R][C] = OUT[C][R] for R < C.  Transpose
+    // reads as in the mirrored store below give each lane OUT[r0 .. r0 + 7][R]; it writes the
+    // entries of row R in columns r0 .. r0 + 7 above the diagonal.  Only entries below the
+    // diagonal are used and only entries above it are written, so no read waits for a write.
+    const int jq16 = lane & 15, g4 = lane >> 4;
+#pragma unroll 2
+    for (int it = 0; it < 32; ++it) {
+      const int blk = it * 4 + wave;
+      const int cb = blk & 15, rb = blk >> 4;
+      const int r0 = 32 * rb + 8 * g4;  // source rows = target columns r0 .. r0 + 7
+      const int R = 16 * cb + jq16;     // target row = source column
+      u32x4 tv;
+      const lds_u8* src = stage_of(r0 >> 6);
+#pragma unroll
+      for (int t4 = 0; t4 < 2; ++t4) {
+        const int r = r0 + 4 * t4 + (jq16 >> 2);
+        const int c = 16 * cb + 4 * (jq16 & 3);
+        const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(src + stage_byte(r, c)));
+        const u32x2 w = __builtin_bit_cast(u32x2, v);
+        tv[2 * t4] = w.x;
+        tv[2 * t4 + 1] = w.y;
+      }
+      if (R < r0 + 7) {  // some column r0 + e lies above the diagonal of row R
+        lds_u8* dst = stage_of(R >> 6) + stage_byte(R, r0);
+        if (R >= r0) {   // the chunk straddles the diagonal: keep columns <= R
+          const u32x4 cur = *reinterpret_cast<const lds_u32x4*>(dst);
+#pragma unroll
+          for (int e2 = 0; e2 < 4; ++e2) {
+            const uint32_t lo = (r0 + 2 * e2 > R) ? (tv[e2] & 0xffffu) : (cur[e2] & 0xffffu);
+            const uint32_t hi = (r0 + 2 * e2 + 1 > R) ? (tv[e2] & 0xffff0000u) : (cur[e2] & 0xffff0000u);
+            tv[e2] = lo | hi;
+          }
+        }
+        *reinterpret_cast<lds_u32x4*>(dst) = tv;
+      }
+    }
+    __syncthreads();
+  }
 
   if (kNN && g.rpart) {
     // Row and column sums of squares of this bf16 output tile, read back from its staged

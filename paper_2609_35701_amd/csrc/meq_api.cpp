@@ -47,9 +47,27 @@ struct MatInfo {
 struct GroupInfo {
   int64_t s, l, S, L;
   std::vector<int> mats;
+  std::vector<int> segs;  // Newton-Schulz schedule: steps per segment (all ones: eq. "ns" as printed)
   size_t off_xa, off_xb, off_a, off_p, off_rpart, off_cpart, off_fold;
+  size_t off_p2, off_t, off_q0, off_q1;  // Gram-space segment buffers (only when a segment has >= 2 / 3 steps)
   int64_t stride_x, stride_a, stride_rpart, stride_cpart;  // elements per matrix
 };
+
+// Segments of the K Newton-Schulz steps of one shape group.  A segment of j steps costs, in
+// s^3 units with r = L / S (symmetric products counted once): X X^T r, the j polynomials j,
+// the 3 (j - 1) products P A, P T, P Q, and Q X 2 r; j single steps cost (3 r + 1) j.  With
+// j >= 2 that is cheaper once r > 1; segments are used from r >= 2 on, where they save at
+// least a quarter of the flops.
+std::vector<int> ns_schedule(int64_t S, int64_t L, int steps, int gram_steps) {
+  const int len = (gram_steps >= 2 && L >= 2 * S) ? gram_steps : 1;
+  std::vector<int> segs;
+  for (int left = steps; left > 0; left -= len) segs.push_back(std::min(len, left));
+  return segs;
+}
+
+// The Newton-Schulz output of a group sits in buffer b after an odd number of segments
+// (each segment ends with one X product that writes the other buffer).
+bool u_in_b(const GroupInfo& g) { return g.segs.size() % 2 == 1; }
 
 struct TimedLaunch {
   int kind;
@@ -85,6 +103,7 @@ meq_status validate_hparams(const meq_hparams& hp) {
   if (!finite(hp.zero_rms_delta) || hp.zero_rms_delta < 0.f) return MEQ_ERR_INVALID_ARG;
   if (hp.nesterov != 0 && hp.nesterov != 1) return MEQ_ERR_INVALID_ARG;
   if (hp.update_rule != MEQ_RULE_MEQMUON && hp.update_rule != MEQ_RULE_MOONLIGHT) return MEQ_ERR_INVALID_ARG;
+  if (hp.ns_gram_steps < 1 || hp.ns_gram_steps > 2) return MEQ_ERR_INVALID_ARG;
   return MEQ_OK;
 }
 
@@ -163,6 +182,7 @@ MEQ_EXPORT void meq_default_hparams(meq_hparams* hp) {
   hp->zero_rms_delta = 1e-7f;
   hp->nesterov = 0;
   hp->update_rule = MEQ_RULE_MEQMUON;
+  hp->ns_gram_steps = 2;
 }
 
 MEQ_EXPORT const char* meq_status_string(meq_status s) {
@@ -245,6 +265,19 @@ meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hpa
     off = align_up(off + 2 * c * g.stride_a, kAlign);
     g.off_p = off;
     off = align_up(off + 2 * c * g.stride_a, kAlign);
+    g.segs = ns_schedule(g.S, g.L, p->hp.ns_steps, p->hp.ns_gram_steps);
+    const int longest = *std::max_element(g.segs.begin(), g.segs.end());
+    g.off_p2 = g.off_t = g.off_q0 = g.off_q1 = 0;
+    if (longest >= 2) {
+      for (size_t* o : {&g.off_p2, &g.off_t, &g.off_q0}) {
+        *o = off;
+        off = align_up(off + 2 * c * g.stride_a, kAlign);
+      }
+    }
+    if (longest >= 3) {
+      g.off_q1 = off;
+      off = align_up(off + 2 * c * g.stride_a, kAlign);
+    }
     g.off_rpart = off;
     off = align_up(off + 4 * c * g.stride_rpart, kAlign);
     g.off_cpart = off;
@@ -345,6 +378,16 @@ MEQ_EXPORT meq_status meq_plan_group(const meq_plan* plan, int32_t g, int64_t* s
   return MEQ_OK;
 }
 
+MEQ_EXPORT meq_status meq_plan_group_schedule(const meq_plan* plan, int32_t g, int32_t* segs, int32_t max_segs,
+                                              int32_t* nsegs) {
+  if (!plan || g < 0 || g >= static_cast<int32_t>(plan->groups.size()) || max_segs < 0 || (max_segs > 0 && !segs))
+    return MEQ_ERR_INVALID_ARG;
+  const std::vector<int>& sg = plan->groups[g].segs;
+  if (nsegs) *nsegs = static_cast<int32_t>(sg.size());
+  for (int32_t i = 0; i < max_segs && i < static_cast<int32_t>(sg.size()); ++i) segs[i] = sg[i];
+  return MEQ_OK;
+}
+
 MEQ_EXPORT meq_status meq_debug_region(const meq_plan* plan, int32_t matrix, int32_t kind, size_t* offset,
                                        int64_t* rows, int64_t* cols, int64_t* ld) {
   if (!plan || matrix < 0 || matrix >= static_cast<int32_t>(plan->mats.size())) return MEQ_ERR_INVALID_ARG;
@@ -373,9 +416,8 @@ MEQ_EXPORT meq_status meq_debug_region(const meq_plan* plan, int32_t matrix, int
   switch (kind) {
     case MEQ_BUF_X0:
     case MEQ_BUF_U: {
-      // X_0 sits in buffer a; iteration k writes buffer b when k is even, so the
-      // output of K steps is in b for odd K and in a for even K.
-      const bool in_b = kind == MEQ_BUF_U && (plan->hp.ns_steps % 2 == 1);
+      // X_0 sits in buffer a; each segment's last product writes the other buffer
+      const bool in_b = kind == MEQ_BUF_U && u_in_b(g);
       o = (in_b ? g.off_xb : g.off_xa) + 2 * static_cast<size_t>(mi.gidx) * g.stride_x;
       r = mi.s;
       c = mi.l;
@@ -560,89 +602,183 @@ meq_status enqueue_prescale(meq_plan* p, char* ws, const void* const* grads, flo
   return MEQ_OK;
 }
 
-// Step a3, iteration k of eq. "ns": per product one launch over all shape groups (chunks of
-// kMaxGemmGroups), longest K first so the long tiles start first.  Ping-pong between buffers
-// a (holding X_0) and b: iteration k reads a when k is even.  With `rowcol` the apply
-// product also writes the row/column sums of squares of its output (step a4's partials).
-meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, bool rowcol, hipStream_t st) {
-  const meq_hparams& hp = p->hp;
-  std::vector<int> order(p->groups.size());
-  for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int>(i);
-  {
-    const bool from_a = (k % 2) == 0;
-    for (int kind = 0; kind < 3; ++kind) {
-      // kind 0: Gram (K = L), 1: polynomial (K = S), 2: apply (K = S)
-      std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
-        const GroupInfo& gx = p->groups[x];
-        const GroupInfo& gy = p->groups[y];
-        const int64_t kx = kind == 0 ? gx.L : gx.S, ky = kind == 0 ? gy.L : gy.S;
-        return kx > ky;
-      });
-      for (size_t c0 = 0; c0 < order.size(); c0 += kMaxGemmGroups) {
-        GemmArgs ga{};
-        ga.count = static_cast<int>(std::min<size_t>(kMaxGemmGroups, order.size() - c0));
-        ga.scale_kind = k == 0 ? (kind == 0 ? 2 : kind == 2 ? 1 : 0) : 0;
-        // The a X term of X <- a X + P X is carried by P: the polynomial product stores
-        // a I + b A + c A A, and the apply product is the plain product (a I + P) X.
-        ga.alpha_e = kind == 1 ? hp.ns_b : 0.f;
-        ga.alpha_acc = kind == 1 ? hp.ns_c : 1.f;
-        ga.alpha_diag = kind == 1 ? hp.ns_a : 0.f;
-        int start = 0;
-        for (int q = 0; q < ga.count; ++q) {
-          const GroupInfo& g = p->groups[order[c0 + q]];
-          const int batch = static_cast<int>(g.mats.size());
-          const int tm = static_cast<int>(g.S / kTile), tn = static_cast<int>(g.L / kTile);
-          uint16_t* cur = reinterpret_cast<uint16_t*>(ws + (from_a ? g.off_xa : g.off_xb));
-          uint16_t* nxt = reinterpret_cast<uint16_t*>(ws + (from_a ? g.off_xb : g.off_xa));
-          uint16_t* am = reinterpret_cast<uint16_t*>(ws + g.off_a);
-          uint16_t* pm = reinterpret_cast<uint16_t*>(ws + g.off_p);
-          GemmGroup& gg = ga.grp[q];
-          gg.fold = reinterpret_cast<const float*>(ws + g.off_fold);
-          if (kind == 0) {  // A = X X^T
-            gg.a = cur; gg.lda = static_cast<int>(g.L); gg.stride_a = g.stride_x;
-            gg.b = cur; gg.ldb = static_cast<int>(g.L); gg.stride_b = g.stride_x;
-            gg.c = am; gg.ldc = static_cast<int>(g.S); gg.stride_c = g.stride_a;
-            gg.e = nullptr; gg.lde = 0; gg.stride_e = 0;
-            gg.K = static_cast<int>(g.L);
-            gg.tiles_m = tm; gg.tiles_n = tm; gg.tiles_per_mat = tm * (tm + 1) / 2;
-          } else if (kind == 1) {  // P = a I + b A + c A A
-            gg.a = am; gg.lda = static_cast<int>(g.S); gg.stride_a = g.stride_a;
-            gg.b = am; gg.ldb = static_cast<int>(g.S); gg.stride_b = g.stride_a;
-            gg.c = pm; gg.ldc = static_cast<int>(g.S); gg.stride_c = g.stride_a;
-            gg.e = am; gg.lde = static_cast<int>(g.S); gg.stride_e = g.stride_a;
-            gg.K = static_cast<int>(g.S);
-            gg.tiles_m = tm; gg.tiles_n = tm; gg.tiles_per_mat = tm * (tm + 1) / 2;
-          } else {  // X <- (a I + b A + c A A) X
-            gg.a = pm; gg.lda = static_cast<int>(g.S); gg.stride_a = g.stride_a;
-            gg.b = cur; gg.ldb = static_cast<int>(g.L); gg.stride_b = g.stride_x;
-            gg.c = nxt; gg.ldc = static_cast<int>(g.L); gg.stride_c = g.stride_x;
-            gg.e = nullptr; gg.lde = 0; gg.stride_e = 0;
-            gg.K = static_cast<int>(g.S);
-            gg.tiles_m = tm; gg.tiles_n = tn; gg.tiles_per_mat = tm * tn;
-            if (rowcol) {
-              gg.rpart = reinterpret_cast<float*>(ws + g.off_rpart);
-              gg.cpart = reinterpret_cast<float*>(ws + g.off_cpart);
-              gg.stride_rpart = g.stride_rpart;
-              gg.stride_cpart = g.stride_cpart;
-            }
-          }
-          gg.tiles = gg.tiles_per_mat * batch;
-          ga.tile_start[q] = start;
-          start += (gg.tiles + 7) / 8 * 8;
-        }
-        ga.tile_start[ga.count] = start;
-        const int kk = kind == 0 ? MEQ_K_GRAM : kind == 1 ? MEQ_K_POLY : MEQ_K_APPLY;
-        MEQ_TRY(timed_launch(p, kk, st, [&] { return launch_gemm(ga, kind, st); }));
+// Step a3 as chains of products, one chain per shape group.  Four product kinds:
+//   OP_GRAM   A <- X X^T                       (symmetric NT kernel, K = L)
+//   OP_POLY   P <- a I + b A + c A A           (symmetric NT kernel with the A tile added, K = S)
+//   OP_SPROD  C <- P M for M in {A, T, Q}      (symmetric NT kernel, K = S; P and M are commuting
+//                                               symmetric matrices, so P M = P M^T is symmetric)
+//   OP_APPLY  X' <- P X or Q X                 (NN kernel, K = S)
+enum OpKind { OP_GRAM = 0, OP_POLY = 1, OP_SPROD = 2, OP_APPLY = 3 };
+
+struct NsOp {
+  int kind;
+  size_t a, b, c, e;  // workspace offsets: operands, output, added tile (OP_POLY)
+  int scale_kind;     // 2: 1/||V||^2 (first X X^T of a step), 1: 1/||V|| (first X product)
+  bool rowcol;        // the step's last X product also writes the row/column sums of squares
+  bool with_prev;     // independent of the previous op of the chain (may share its launch)
+};
+
+// One shape group's products over a schedule.  A segment of j steps is eq. "ns" regrouped:
+// A = X X^T once; for each step P_i = a I + b A + c A A, then (before the segment's last
+// step) A <- P_i (P_i A), since X P-updated gives (P X)(P X)^T = P A P = P P A; the
+// segment's product Q = P_last ... P_first accumulates alongside; finally X <- Q X.  A
+// one-step segment is exactly A = X X^T, P, X <- P X.  X_0 is in buffer a when x_in_a.
+std::vector<NsOp> group_ops(const GroupInfo& g, const std::vector<int>& segs, bool x_in_a, bool first_fold,
+                            bool rowcol) {
+  std::vector<NsOp> ops;
+  size_t cur = x_in_a ? g.off_xa : g.off_xb, nxt = x_in_a ? g.off_xb : g.off_xa;
+  const size_t pbuf[2] = {g.off_p, g.off_p2}, qbuf[2] = {g.off_q0, g.off_q1};
+  for (size_t si = 0; si < segs.size(); ++si) {
+    const bool fold = first_fold && si == 0;
+    ops.push_back({OP_GRAM, cur, cur, g.off_a, 0, fold ? 2 : 0, false, false});
+    size_t q = 0;
+    for (int j = 0; j < segs[si]; ++j) {
+      const size_t pj = pbuf[j % 2];
+      ops.push_back({OP_POLY, g.off_a, g.off_a, pj, g.off_a, 0, false, false});
+      if (j == 0) {
+        q = pj;
+      } else {  // Q <- P_j Q (reads the other P buffer or a Q buffer, writes the free Q buffer)
+        const size_t qn = qbuf[(j - 1) % 2];
+        ops.push_back({OP_SPROD, pj, q, qn, 0, 0, false, false});
+        q = qn;
+      }
+      if (j + 1 < segs[si]) {
+        ops.push_back({OP_SPROD, pj, g.off_a, g.off_t, 0, 0, false, j > 0});  // T <- P_j A
+        ops.push_back({OP_SPROD, pj, g.off_t, g.off_a, 0, 0, false, false});  // A <- P_j T
       }
     }
+    ops.push_back({OP_APPLY, q, cur, nxt, 0, fold ? 1 : 0, rowcol && si + 1 == segs.size(), false});
+    std::swap(cur, nxt);
   }
-  return MEQ_OK;
+  return ops;
 }
 
-// Steps a4-a5 on the Newton-Schulz output in buffer b (u_in_b) or a: row/column RMS, CVs,
-// direction and scale vectors; with the Moonlight rule only the uniform scale.  With
-// `sums_done` the row/column sums of squares were already written by the last apply product.
-meq_status enqueue_stats(meq_plan* p, char* ws, bool u_in_b, bool moonlight, bool sums_done, hipStream_t st) {
+// Fill one launch entry for op `op` of shape group g.
+void fill_gemm_group(GemmGroup& gg, const NsOp& op, const GroupInfo& g, char* ws) {
+  auto buf = [&](size_t off) { return reinterpret_cast<uint16_t*>(ws + off); };
+  const int tm = static_cast<int>(g.S / kTile), tn = static_cast<int>(g.L / kTile);
+  const int S = static_cast<int>(g.S), L = static_cast<int>(g.L);
+  gg = GemmGroup{};
+  gg.fold = reinterpret_cast<const float*>(ws + g.off_fold);
+  gg.scale_kind = op.scale_kind;
+  gg.a = buf(op.a);
+  gg.c = buf(op.c);
+  if (op.kind == OP_APPLY) {
+    gg.lda = S; gg.stride_a = g.stride_a;
+    gg.b = buf(op.b); gg.ldb = L; gg.stride_b = g.stride_x;
+    gg.ldc = L; gg.stride_c = g.stride_x;
+    gg.K = S;
+    gg.tiles_m = tm; gg.tiles_n = tn; gg.tiles_per_mat = tm * tn;
+    if (op.rowcol) {
+      gg.rpart = reinterpret_cast<float*>(ws + g.off_rpart);
+      gg.cpart = reinterpret_cast<float*>(ws + g.off_cpart);
+      gg.stride_rpart = g.stride_rpart;
+      gg.stride_cpart = g.stride_cpart;
+    }
+  } else {
+    const bool gram = op.kind == OP_GRAM;
+    gg.lda = gram ? L : S; gg.stride_a = gram ? g.stride_x : g.stride_a;
+    gg.b = buf(op.b); gg.ldb = gg.lda; gg.stride_b = gg.stride_a;
+    gg.ldc = S; gg.stride_c = g.stride_a;
+    if (op.kind == OP_POLY) {
+      gg.e = buf(op.e); gg.lde = S; gg.stride_e = g.stride_a;
+    }
+    gg.K = gram ? L : S;
+    gg.symmetrize = op.kind == OP_SPROD;
+    gg.tiles_m = tm; gg.tiles_n = tm; gg.tiles_per_mat = tm * (tm + 1) / 2;
+  }
+  gg.tiles = gg.tiles_per_mat * static_cast<int>(g.mats.size());
+}
+
+// Enqueue the chains of all groups.  Launch by launch, pick the op kind with the most work
+// (tiles x K) among the chains' next ops and run every chain's next op of that kind (and the
+// ops after it that are independent of it and of the same kind) in grouped launches of up
+// to kMaxGemmGroups entries, longest K first so the long tiles start first.
+meq_status enqueue_chains(meq_plan* p, char* ws, const std::vector<std::vector<NsOp>>& chains, hipStream_t st) {
+  const meq_hparams& hp = p->hp;
+  std::vector<size_t> head(chains.size(), 0);
+  auto work = [&](size_t gi, const NsOp& op) {
+    const GroupInfo& g = p->groups[gi];
+    const double tm = static_cast<double>(g.S / kTile);
+    const double tiles = op.kind == OP_APPLY ? tm * static_cast<double>(g.L / kTile) : tm * (tm + 1) / 2;
+    return tiles * static_cast<double>(g.mats.size()) * static_cast<double>(op.kind == OP_GRAM ? g.L : g.S);
+  };
+  for (;;) {
+    double best = -1.0;
+    int kind = -1;
+    for (int k = 0; k < 4; ++k) {
+      double w = 0.0;
+      bool any = false;
+      for (size_t gi = 0; gi < chains.size(); ++gi)
+        if (head[gi] < chains[gi].size() && chains[gi][head[gi]].kind == k) {
+          w += work(gi, chains[gi][head[gi]]);
+          any = true;
+        }
+      if (any && w > best) {
+        best = w;
+        kind = k;
+      }
+    }
+    if (kind < 0) return MEQ_OK;
+    std::vector<std::pair<size_t, const NsOp*>> entries;
+    for (size_t gi = 0; gi < chains.size(); ++gi) {
+      if (head[gi] >= chains[gi].size() || chains[gi][head[gi]].kind != kind) continue;
+      entries.push_back({gi, &chains[gi][head[gi]++]});
+      while (head[gi] < chains[gi].size() && chains[gi][head[gi]].with_prev && chains[gi][head[gi]].kind == kind)
+        entries.push_back({gi, &chains[gi][head[gi]++]});
+    }
+    std::stable_sort(entries.begin(), entries.end(), [&](const auto& x, const auto& y) {
+      const GroupInfo& gx = p->groups[x.first];
+      const GroupInfo& gy = p->groups[y.first];
+      return (kind == OP_GRAM ? gx.L : gx.S) > (kind == OP_GRAM ? gy.L : gy.S);
+    });
+    const int mode = kind == OP_POLY ? 1 : kind == OP_APPLY ? 2 : 0;
+    const int tk = kind == OP_GRAM ? MEQ_K_GRAM : kind == OP_POLY ? MEQ_K_POLY
+                 : kind == OP_APPLY ? MEQ_K_APPLY : MEQ_K_GRAM_SPACE;
+    for (size_t c0 = 0; c0 < entries.size(); c0 += kMaxGemmGroups) {
+      GemmArgs ga{};
+      ga.count = static_cast<int>(std::min<size_t>(kMaxGemmGroups, entries.size() - c0));
+      // The a X term of X <- a X + P X is carried by P: the polynomial product stores
+      // a I + b A + c A A, and the X product is the plain product P X.
+      ga.alpha_e = kind == OP_POLY ? hp.ns_b : 0.f;
+      ga.alpha_acc = kind == OP_POLY ? hp.ns_c : 1.f;
+      ga.alpha_diag = kind == OP_POLY ? hp.ns_a : 0.f;
+      int start = 0;
+      for (int q = 0; q < ga.count; ++q) {
+        fill_gemm_group(ga.grp[q], *entries[c0 + q].second, p->groups[entries[c0 + q].first], ws);
+        ga.tile_start[q] = start;
+        start += (ga.grp[q].tiles + 7) / 8 * 8;
+      }
+      ga.tile_start[ga.count] = start;
+      MEQ_TRY(timed_launch(p, tk, st, [&] { return launch_gemm(ga, mode, st); }));
+    }
+  }
+}
+
+// Step a3 of a full step: every group over its own schedule, X_0 in buffer a, the prescale
+// folded into the first products; with `rowcol` the last X product also writes the row/column
+// sums of squares of its output (step a4's partials).
+meq_status enqueue_ns(meq_plan* p, char* ws, bool rowcol, hipStream_t st) {
+  std::vector<std::vector<NsOp>> chains;
+  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, g.segs, true, true, rowcol));
+  return enqueue_chains(p, ws, chains, st);
+}
+
+// One step k of eq. "ns" as printed for every group (the CV trace replays the iterates one by
+// one): iteration k reads buffer a when k is even.
+meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, hipStream_t st) {
+  std::vector<std::vector<NsOp>> chains;
+  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, {1}, k % 2 == 0, k == 0, false));
+  return enqueue_chains(p, ws, chains, st);
+}
+
+// Steps a4-a5 on the Newton-Schulz output: row/column RMS, CVs, direction and scale vectors;
+// with the Moonlight rule only the uniform scale.  With `sums_done` the row/column sums of
+// squares were already written by the last X product.  The output sits where each group's
+// schedule left it, or, for the CV trace's replayed iterates, in buffer b when trace_in_b > 0
+// and a when it is 0.
+meq_status enqueue_stats(meq_plan* p, char* ws, bool moonlight, bool sums_done, hipStream_t st,
+                         int trace_in_b = -1) {
   const meq_hparams& hp = p->hp;
   const int count = static_cast<int>(p->mats.size());
   MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
@@ -654,7 +790,7 @@ meq_status enqueue_stats(meq_plan* p, char* ws, bool u_in_b, bool moonlight, boo
     uint16_t* xa = reinterpret_cast<uint16_t*>(ws + g.off_xa);
     uint16_t* xb = reinterpret_cast<uint16_t*>(ws + g.off_xb);
     RowColArgs rc{};
-    rc.u = u_in_b ? xb : xa;
+    rc.u = (trace_in_b >= 0 ? trace_in_b > 0 : u_in_b(g)) ? xb : xa;
     rc.stride_u = g.stride_x;
     rc.S = static_cast<int>(g.S);
     rc.L = static_cast<int>(g.L);
@@ -724,7 +860,7 @@ meq_status enqueue_update(meq_plan* p, char* ws, void* const* params, float lr, 
       a.ldu[k] = g.L;
       a.w[k] = params[ch[k]];
       a.vec[k] = (mi.n % 8 == 0) && aligned(a.w[k], 16);
-      const size_t uoff = (hp.ns_steps % 2 == 1) ? g.off_xb : g.off_xa;
+      const size_t uoff = u_in_b(g) ? g.off_xb : g.off_xa;
       a.u[k] = reinterpret_cast<const uint16_t*>(ws + uoff) + mi.gidx * g.stride_x;
       a.scale[k] = reinterpret_cast<const float*>(ws + mi.off_scale);
       a.scal[k] = scal + ch[k];
@@ -757,9 +893,8 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     const meq_hparams& hp = p->hp;
     const bool moonlight = hp.update_rule == MEQ_RULE_MOONLIGHT;
     MEQ_TRY(enqueue_prescale(p, ws, grads, momenta, st));
-    for (int k = 0; k < hp.ns_steps; ++k)
-      MEQ_TRY(enqueue_ns_iteration(p, ws, k, !moonlight && k == hp.ns_steps - 1, st));
-    MEQ_TRY(enqueue_stats(p, ws, hp.ns_steps % 2 == 1, moonlight, !moonlight, st));
+    MEQ_TRY(enqueue_ns(p, ws, !moonlight, st));
+    MEQ_TRY(enqueue_stats(p, ws, moonlight, !moonlight, st));
     MEQ_TRY(enqueue_update(p, ws, params, lr, st));
     return MEQ_OK;
   });
@@ -781,9 +916,9 @@ MEQ_EXPORT meq_status meq_ns_cv_trace(meq_plan* p, const void* const* inputs, in
     const char* src = ws + p->off_scal;
     MEQ_TRY(enqueue_prescale(p, ws, inputs, nullptr, st));
     for (int k = 0; k <= kmax; ++k) {
-      if (k > 0) MEQ_TRY(enqueue_ns_iteration(p, ws, k - 1, false, st));
+      if (k > 0) MEQ_TRY(enqueue_ns_iteration(p, ws, k - 1, st));
       // X_0 (unscaled V: CVs are scale free) sits in buffer a; iteration k - 1 writes b for odd k
-      MEQ_TRY(enqueue_stats(p, ws, k % 2 == 1, false, false, st));
+      MEQ_TRY(enqueue_stats(p, ws, false, false, st, k % 2 == 1));
       if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
         return MEQ_ERR_HIP;
       if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;

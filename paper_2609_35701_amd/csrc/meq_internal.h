@@ -60,7 +60,8 @@ struct NormArgs {
 // matrices of a shape group; one launch covers up to kMaxGemmGroups groups.  Aop is
 // M x K row-major.  Bop is N x K row-major (NT) or K x N row-major (NN).  For the
 // symmetric products only tiles on or above the diagonal are computed and each
-// off-diagonal tile is also stored mirrored.
+// off-diagonal tile is also stored mirrored: Aop . Bop^T must be symmetric (X X^T, or
+// the product of two commuting symmetric matrices, where Bop^T = Bop).
 constexpr int kMaxGemmGroups = 8;
 
 struct GemmGroup {
@@ -74,6 +75,8 @@ struct GemmGroup {
   int K;
   int tiles_m, tiles_n, tiles_per_mat;
   int tiles;           // batch * tiles_per_mat
+  int scale_kind;      // 0 none, 1 scale by 1/||V||, 2 scale by 1/||V||^2 (first products of a step)
+  int symmetrize;      // symmetric products of two different factors: make diagonal tiles exactly symmetric
   // apply product only, when not null: sums of squares of the bf16 output per row of each
   // 256-column tile (rpart, (L/256) x S per matrix) and per column of each 256-row tile
   // (cpart, (S/256) x L per matrix), the partials of eq. "row-col-rms" for the last iteration
@@ -84,7 +87,6 @@ struct GemmGroup {
 
 struct GemmArgs {
   int count;                             // groups in this launch
-  int scale_kind;                        // 0 none, 1 scale by 1/||V||, 2 scale by 1/||V||^2
   float alpha_e, alpha_acc;
   float alpha_diag;                      // symmetric products only
   int tile_start[kMaxGemmGroups + 1];    // workgroup ranges per group, multiples of 8

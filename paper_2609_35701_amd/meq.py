@@ -20,13 +20,13 @@ PARAM_HIDDEN, PARAM_AUX, PARAM_VECTOR = 0, 1, 2
 RULE_MEQMUON, RULE_MOONLIGHT = 0, 1
 BUF_X0, BUF_U, BUF_NORMSQ, BUF_ROW_RMS, BUF_COL_RMS, BUF_SCALE = range(6)
 (K_MOMENTUM, K_NORM, K_GRAM, K_POLY, K_APPLY, K_ROWCOL, K_SELECT, K_UPDATE,
- K_AUX_ROWS, K_AUX_COLS, K_AUX_UPDATE, K_VECTOR) = range(12)
+ K_AUX_ROWS, K_AUX_COLS, K_AUX_UPDATE, K_VECTOR, K_GRAM_SPACE) = range(13)
 KERNEL_NAMES = ("momentum", "norm", "gram", "poly", "apply", "rowcol", "select", "update",
-                "aux_rows", "aux_cols", "aux_update", "vector")
+                "aux_rows", "aux_cols", "aux_update", "vector", "gram_space")
 
 EXPORTED = ("meq_default_hparams", "meq_init", "meq_init_kind", "meq_workspace_bytes", "meq_step",
             "meq_get_stats", "meq_ns_cv_trace", "meq_destroy", "meq_status_string", "meq_plan_num_groups", "meq_plan_group",
-            "meq_debug_region", "meq_set_timing", "meq_get_timing")
+            "meq_plan_group_schedule", "meq_debug_region", "meq_set_timing", "meq_get_timing")
 
 
 class MeqLibraryMissing(RuntimeError):
@@ -43,7 +43,7 @@ class HParams(ctypes.Structure):
     _fields_ = [("mu", ctypes.c_float), ("rho", ctypes.c_float), ("weight_decay", ctypes.c_float),
                 ("ns_steps", ctypes.c_int32), ("ns_a", ctypes.c_float), ("ns_b", ctypes.c_float),
                 ("ns_c", ctypes.c_float), ("zero_rms_delta", ctypes.c_float), ("nesterov", ctypes.c_int32),
-                ("update_rule", ctypes.c_int32)]
+                ("update_rule", ctypes.c_int32), ("ns_gram_steps", ctypes.c_int32)]
 
 
 class MatrixDesc(ctypes.Structure):
@@ -87,6 +87,8 @@ def lib() -> ctypes.CDLL:
     L.meq_plan_num_groups.restype = c_i32
     L.meq_plan_group.argtypes = [vp, c_i32, ctypes.POINTER(c_i64), ctypes.POINTER(c_i64), ctypes.POINTER(c_i32)]
     L.meq_plan_group.restype = c_i32
+    L.meq_plan_group_schedule.argtypes = [vp, c_i32, ctypes.POINTER(c_i32), c_i32, ctypes.POINTER(c_i32)]
+    L.meq_plan_group_schedule.restype = c_i32
     L.meq_debug_region.argtypes = [vp, c_i32, c_i32, ctypes.POINTER(c_sz), ctypes.POINTER(c_i64),
                                    ctypes.POINTER(c_i64), ctypes.POINTER(c_i64)]
     L.meq_debug_region.restype = c_i32
@@ -172,6 +174,15 @@ class Plan:
             _check(L.meq_plan_group(self._h, g, ctypes.byref(s), ctypes.byref(l), ctypes.byref(c)), "meq_plan_group")
             out.append((s.value, l.value, c.value))
         return out
+
+    def schedule(self, group: int) -> List[int]:
+        """Steps per Newton-Schulz segment of shape group ``group`` (``meq_plan_group_schedule``)."""
+        L = lib()
+        n = ctypes.c_int32()
+        _check(L.meq_plan_group_schedule(self._h, group, None, 0, ctypes.byref(n)), "meq_plan_group_schedule")
+        segs = (ctypes.c_int32 * max(n.value, 1))()
+        _check(L.meq_plan_group_schedule(self._h, group, segs, n.value, ctypes.byref(n)), "meq_plan_group_schedule")
+        return list(segs)[:n.value]
 
     def debug_region(self, matrix: int, kind: int):
         """(byte offset, rows, cols, ld) of a workspace buffer (``meq_debug_region``)."""

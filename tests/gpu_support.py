@@ -61,6 +61,15 @@ def ulp_bf16(x: np.ndarray) -> np.ndarray:
     return np.ldexp(1.0, np.maximum(e, -125) - 8)
 
 
+def schedule_of(plan: meq.Plan, shape) -> list:
+    """Newton-Schulz segments of the shape group a matrix of `shape` belongs to."""
+    key = (min(shape), max(shape))
+    for g, (s, l, _) in enumerate(plan.groups()):
+        if (s, l) == key:
+            return plan.schedule(g)
+    raise KeyError(shape)
+
+
 class Run:
     """Matrices of a workload on the GPU, stepped through the HIP path."""
 
@@ -109,8 +118,8 @@ def check_matrix_step(run: Run, k: int, w_before: np.ndarray, b_before: np.ndarr
     nsq_or = float(np.sum(v_or * v_or))
     assert abs(nsq_gpu - nsq_or) <= TOL_FP32 * max(nsq_or, 1e-300), f"{label}: normsq {nsq_gpu} vs {nsq_or}"
     x0_or = oracle.round_bf16(wide(v_or))
-    if run.hp.ns_steps == 1:
-        # the X_0 buffer survives the step only with one Newton-Schulz step
+    if len(schedule_of(upd.plan, w_before.shape)) == 1:
+        # the X_0 buffer survives the step only when the matrix's schedule has one segment
         x0_gpu = to_np(upd.view(k, meq.BUF_X0))
         diff = np.abs(x0_gpu - x0_or)
         assert np.all(diff <= ulp_bf16(x0_or) + 1e-300), f"{label}: bf16 V off by more than one ulp"
