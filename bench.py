@@ -114,8 +114,23 @@ def summarize_traffic(fetch_dir: str, write_dir: str, out: str, fetch_cmd: str, 
         f.write("".join(lines))
 
 
-def summarize_stats(stats_csv: str, out: str, command: str, note: str) -> None:
-    """Markdown table of a rocprofv3 --kernel-trace --stats run."""
+def timed_region_average(trace_csv: str, line: dict, kernel: str = "k_ns_gemm<2>") -> tuple:
+    """Average duration (ms) and count of `kernel`'s dispatches inside the benchmark's timed region,
+    from a rocprofv3 kernel trace of the same run: the main plan runs warmup + steps steps first,
+    with roofline.launches_per_step launches of the kernel each; later legs follow them."""
+    with open(trace_csv) as f:
+        rows = [r for r in csv.DictReader(f) if _kernel_key(r["Kernel_Name"]) == kernel]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    per = int(round(line["roofline"]["launches_per_step"]))
+    lo, hi = line["warmup"] * per, (line["warmup"] + line["steps"]) * per
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6 for r in rows[lo:hi]]
+    return sum(durs) / len(durs), len(durs)
+
+
+def summarize_stats(stats_csv: str, out: str, command: str, note: str, trace_csv: str = None,
+                    bench_json: str = None) -> None:
+    """Markdown table of a rocprofv3 --kernel-trace --stats run; with the run's kernel trace and
+    bench line, also the apply kernel's timed-region average next to the bench's HIP-event figure."""
     with open(stats_csv) as f:
         rows = list(csv.DictReader(f))
 
@@ -129,11 +144,26 @@ def summarize_stats(stats_csv: str, out: str, command: str, note: str) -> None:
              f"    {command}\n\n"]
     if note:
         lines.append(note + "\n\n")
+    if trace_csv and bench_json:
+        with open(bench_json) as f:
+            line = json.loads([x for x in f if x.startswith("{")][-1])
+        avg, n = timed_region_average(trace_csv, line)
+        lines.append(
+            f"Timed region of the same run (summarised with `python bench.py --summarize-stats <stats csv> "
+            f"--trace <trace csv> --bench-json <bench line> --out <this file>`): {line['steps']} steps after "
+            f"{line['warmup']} warm-up steps, {line['ms_per_step']:.3f} ms/step under the profiler; the apply "
+            f"product k_ns_gemm<2> launches {line['roofline']['launches_per_step']:g} times per step. Its "
+            f"average over the {n} timed-region dispatches in the rocprofv3 trace is {avg:.4f} ms; the "
+            f"bench line reports {line['roofline']['avg_launch_ms']:.4f} ms from HIP events on its launch "
+            "stream. The table below averages every dispatch of the run, including the legs after the "
+            "timed region (other parameter kinds, the Moonlight-Muon rule and the printed iteration on the "
+            "same kernels, the library GEMM), so its per-kernel averages mix launch shapes.\n\n")
     lines.append("| kernel | calls | total ms | avg ms | min ms | max ms | % |\n|---|---|---|---|---|---|---|\n")
     for r in rows:
         lines.append(f"| {short(r['Name'])} | {r['Calls']} | {int(r['TotalDurationNs']) / 1e6:.3f} | "
                      f"{float(r['AverageNs']) / 1e6:.4f} | {int(r['MinNs']) / 1e6:.4f} | "
                      f"{int(r['MaxNs']) / 1e6:.4f} | {float(r['Percentage']):.2f} |\n")
+    lines.append(f"\nkernel_source_sha256: {gemm_source_hash()}\n")
     with open(out, "w") as f:
         f.write("".join(lines))
 
@@ -169,35 +199,42 @@ def ns_launch_flops(wl) -> dict:
     return out
 
 
-def summarize_mfma(run_dir: str, out: str, command: str, workload: str, note: str) -> None:
-    """Matrix-core utilisation of the NS products from one rocprofv3 --pmc run of MFMA_COUNTERS."""
+def _counter_totals(run_dir: str, counter: str):
+    """Sum of one rocprofv3 --pmc counter over all dispatches, and the dispatch count, by kernel."""
+    return {k: (mean * n, n) for k, (mean, n) in _counter_means(run_dir, counter).items()}
+
+
+def summarize_mfma(run_dir: str, out: str, command: str, workload: str, note: str, steps: int) -> None:
+    """Matrix-core utilisation of the NS products from one rocprofv3 --pmc run of MFMA_COUNTERS
+    covering `steps` meq_step calls (warm-up included)."""
     import workloads
 
     wl = workloads.workload(workload)
     flops = ns_launch_flops(wl)
-    means = {c: _counter_means(run_dir, c) for c in MFMA_COUNTERS}
+    tot = {c: _counter_totals(run_dir, c) for c in MFMA_COUNTERS}
     lines = [
         f"# Matrix-core counters of the Newton-Schulz products, {workload} step\n\n",
         "Command (from the repository root on one MI355X):\n\n", f"    {command}\n\n",
-        f"Summarised with `python bench.py --summarize-mfma <dir> --out <this file>`.  Per dispatch: "
-        "GRBM_GUI_ACTIVE summed over the 8 XCDs (divided by 8: cycles the kernel was active); "
-        f"SQ_VALU_MFMA_BUSY_CYCLES summed over all {SIMDS} SIMDs (divided by {SIMDS} and by the active cycles: "
-        "fraction of the time a SIMD's matrix core was busy); SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 = bf16 "
-        "flops the matrix cores executed, against the flops the 256 x 256 tiles execute by count "
-        "(padding and the lower half of diagonal tiles of the symmetric products included) and the "
-        "algorithmic symmetric-aware flops.\n\n",
+        f"Summarised with `python bench.py --summarize-mfma <dir> --profiled-steps {steps} --out <this file>`. "
+        f"Per step ({steps} meq_step calls in the run, warm-up included): GRBM_GUI_ACTIVE summed over the 8 XCDs "
+        f"(divided by 8: cycles the kernel template was active); SQ_VALU_MFMA_BUSY_CYCLES summed over all {SIMDS} "
+        f"SIMDs (divided by {SIMDS} and by the active cycles: fraction of the time a SIMD's matrix core was busy); "
+        "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 = bf16 flops the matrix cores executed, against the flops the "
+        "256 x 256 tiles execute by count (padding and the lower half of diagonal tiles of the symmetric "
+        "products included) and the algorithmic symmetric-aware flops of the step's schedule. "
+        "k_ns_gemm<0> covers both X X^T and the Gram-space products P A, P T, P Q.\n\n",
         (note + "\n\n" if note else ""),
-        "| kernel | dispatches | active cycles | MFMA busy | MOPS x 512 | tile flops | algorithmic flops | "
-        "MOPS x 512 / tile flops |\n",
+        "| kernel | dispatches per step | active cycles per step | MFMA busy | MOPS x 512 per step | tile flops "
+        "per step | algorithmic flops per step | MOPS x 512 / tile flops |\n",
         "|---|---|---|---|---|---|---|---|\n",
     ]
     for k in ("k_ns_gemm<0>", "k_ns_gemm<1>", "k_ns_gemm<2>"):
-        gui, n = means["GRBM_GUI_ACTIVE"].get(k, (float("nan"), 0))
-        cyc = gui / XCDS
-        busy = means["SQ_VALU_MFMA_BUSY_CYCLES"].get(k, (float("nan"), 0))[0] / SIMDS / cyc
-        mops = means["SQ_INSTS_VALU_MFMA_MOPS_BF16"].get(k, (float("nan"), 0))[0] * 512
+        gui, n = tot["GRBM_GUI_ACTIVE"].get(k, (float("nan"), 0))
+        cyc = gui / XCDS / steps
+        busy = tot["SQ_VALU_MFMA_BUSY_CYCLES"].get(k, (float("nan"), 0))[0] / SIMDS / steps / cyc
+        mops = tot["SQ_INSTS_VALU_MFMA_MOPS_BF16"].get(k, (float("nan"), 0))[0] * 512 / steps
         alg, exe = flops[k]
-        lines.append(f"| {k} | {n} | {cyc:.4g} | {busy:.1%} | {mops:.4g} | {exe:.4g} | {alg:.4g} | "
+        lines.append(f"| {k} | {n / steps:.4g} | {cyc:.4g} | {busy:.1%} | {mops:.4g} | {exe:.4g} | {alg:.4g} | "
                      f"{mops / exe:.4f} |\n")
     lines.append(f"\nkernel_source_sha256: {gemm_source_hash()}\n")
     with open(out, "w") as f:
@@ -435,6 +472,10 @@ def main() -> int:
                     help="summarise a rocprofv3 --kernel-trace --stats run into --out and exit")
     ap.add_argument("--summarize-mfma", metavar="PMC_DIR",
                     help="summarise a rocprofv3 --pmc run of the matrix-core counters into --out and exit")
+    ap.add_argument("--trace", help="rocprofv3 kernel trace csv of the --summarize-stats run")
+    ap.add_argument("--bench-json", help="the bench line printed by the --summarize-stats run")
+    ap.add_argument("--profiled-steps", type=int, default=3,
+                    help="meq_step calls (warm-up included) in the run --summarize-mfma reads")
     ap.add_argument("--out")
     ap.add_argument("--command", default="", help="command line(s) recorded in a summary ('|' separates two)")
     ap.add_argument("--note", default="")
@@ -445,10 +486,10 @@ def main() -> int:
                           cmds[1].strip())
         return 0
     if args.summarize_stats:
-        summarize_stats(args.summarize_stats, args.out, args.command, args.note)
+        summarize_stats(args.summarize_stats, args.out, args.command, args.note, args.trace, args.bench_json)
         return 0
     if args.summarize_mfma:
-        summarize_mfma(args.summarize_mfma, args.out, args.command, args.workload, args.note)
+        summarize_mfma(args.summarize_mfma, args.out, args.command, args.workload, args.note, args.profiled_steps)
         return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the MeqMuon update is measured on a single MI355X; "
@@ -517,6 +558,7 @@ def main() -> int:
                 "achieved": apply_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": apply_tflops / PEAK_BF16_TFLOPS, "traffic": recorded_traffic(wl.name),
                 "flops_per_launch": fl["apply"] / max(kern["apply"]["launches_per_step"], 1),
+                "launches_per_step": kern["apply"]["launches_per_step"],
                 "avg_launch_ms": kern["apply"]["avg_launch_ms"]}
     stages = {
         "ns_tflops": fl["total"] / (ns_ms * 1e-3) / 1e12,
