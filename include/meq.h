@@ -82,22 +82,22 @@ typedef enum { MEQ_RULE_MEQMUON = 0, MEQ_RULE_MOONLIGHT = 1 } meq_update_rule;
  *   nesterov       0: normalize B_t (Algorithm "MeqMuon");
  *                  1: normalize G_t + mu * B_t (the experiments' hidden weights)
  *   update_rule    meq_update_rule; MEQ_RULE_MOONLIGHT only for MEQ_PARAM_HIDDEN plans
- *   ns_gram_steps  g, 1 <= g <= 2: the most Newton-Schulz steps one Gram-space segment
+ *   ns_gram_steps  g, 1 <= g <= 3: the most Newton-Schulz steps one Gram-space segment
  *                  covers.  g = 1 runs eq. "ns" as printed: every step forms A = X X^T,
- *                  the polynomial P = a I + b A + c A A and X <- P X.  With g = 2, a
- *                  matrix whose padded long side is at least twice its padded short side
- *                  runs its K steps in segments of at most 2 steps: a segment forms
- *                  A = X X^T once, then iterates on s x s matrices only (each step's P is a
- *                  polynomial of A, so A_{k+1} = P_k A_k P_k, and the segment's product
- *                  Q = P_{k+1} P_k is symmetric), and ends with one product X <- Q X.
- *                  Equal to eq. "ns" in exact arithmetic; it replaces most s x l products
- *                  by s x s ones.  Segments are 2 steps long, the last one takes the
- *                  remainder (K = 5: 2 + 2 + 1).  Default 2.  Longer segments are not
- *                  offered: in bf16, A = X X^T squares the spread of the singular values and
- *                  the segment's rounding errors are not corrected by later printed steps;
- *                  3 + 2 reaches about 3% relative error in the Newton-Schulz output on
- *                  small ill-conditioned inputs, at the 3e-2 bound that 2 + 2 + 1 meets with
- *                  room to spare (about 1.3%, against about 0.9% for the printed iteration).
+ *                  the polynomial P = a I + b A + c A A and X <- P X (bf16 operands,
+ *                  fp32 accumulation).  With g >= 2, a matrix whose padded long side is
+ *                  at least twice its padded short side runs its K steps in segments of at
+ *                  most g steps: a segment forms A = X X^T once, then iterates on s x s
+ *                  matrices only (each step's P is a polynomial of A, so
+ *                  A_{k+1} = P_k A_k P_k and the segment's product Q = P_last ... P_first
+ *                  are symmetric and commute), and ends with one product X <- Q X.  The
+ *                  s x s matrices of a segment are held in fp16 (A scaled by 2^13), whose
+ *                  11-bit significand keeps the regrouped iteration at least as accurate as
+ *                  the printed bf16 step; X and the final Q are bf16.  Equal to eq. "ns" in
+ *                  exact arithmetic; it replaces most s x l products by s x s ones.
+ *                  Segments are g steps long, the last one takes the remainder (K = 5,
+ *                  g = 3: 3 + 2).  Default 3.  Longer segments are not offered: a single
+ *                  segment of 4 or 5 steps loses accuracy on rank-deficient inputs.
  * ns_steps, ns_a/b/c and ns_gram_steps only matter for hidden plans but are validated for
  * every plan.
  */
@@ -136,7 +136,7 @@ typedef struct meq_plan meq_plan; /* opaque; owns host metadata only */
 
 /* Fill *hp with the paper's defaults: mu 0.95, rho 0.2, lambda 0.1, K 5,
  * (a, b, c) = (3.4445, -4.7750, 2.0315), delta 1e-7, nesterov 0,
- * update_rule MEQ_RULE_MEQMUON, ns_gram_steps 2.  No-op on null. */
+ * update_rule MEQ_RULE_MEQMUON, ns_gram_steps 3.  No-op on null. */
 void meq_default_hparams(meq_hparams* hp);
 
 /*
@@ -260,7 +260,8 @@ meq_status meq_debug_region(const meq_plan* plan, int32_t matrix, int32_t kind, 
 typedef enum {
   MEQ_K_MOMENTUM = 0, /* momentum + ||V||^2 partials + bf16 V in wide orientation            */
   MEQ_K_NORM = 1,     /* ||V||_F^2 finalization                                                */
-  MEQ_K_GRAM = 2,     /* A = X X^T (symmetric tiles)                                           */
+  MEQ_K_GRAM = 2,     /* A = X X^T and the Gram-space products P A, P T, P Q (symmetric tiles;  */
+                      /* one launch may carry both)                                            */
   MEQ_K_POLY = 3,     /* P = a I + b A + c A A (symmetric tiles)                               */
   MEQ_K_APPLY = 4,    /* X <- P X, or X <- Q X at the end of a Gram-space segment              */
   MEQ_K_ROWCOL = 5,   /* row and column sums of squares of U                                    */
@@ -270,8 +271,7 @@ typedef enum {
   MEQ_K_AUX_COLS = 9,   /* aux: column RMS of N_r(V) (partials + finalization)                   */
   MEQ_K_AUX_UPDATE = 10, /* aux: decoupled weight decay + two-sided normalized update            */
   MEQ_K_VECTOR = 11,    /* vector: momentum, global RMS and write-back in one kernel             */
-  MEQ_K_GRAM_SPACE = 12, /* Gram-space segment products P A, P T, P Q (symmetric tiles)         */
-  MEQ_K_COUNT = 13
+  MEQ_K_COUNT = 12
 } meq_kernel_kind;
 
 /* Bracket every launch of the kinds in `kind_mask` (bit k = meq_kernel_kind k)

@@ -20,6 +20,8 @@
 // conflicts.  The epilogue stages the output tile (and, for P, the A tile it adds) in
 // LDS and writes whole rows with 16-byte stores.  Same-shape matrices form one
 // launch; workgroup ids are remapped so each XCD receives a contiguous run of tiles.
+#include <type_traits>
+
 #include "meq_internal.h"
 
 namespace meq {
@@ -28,6 +30,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -43,10 +47,18 @@ typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 constexpr int kBufferFlags = 0x00020000;
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+__device__ __forceinline__ float f16_to_f32(uint32_t h) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h)));
+}
 
 // Two floats -> packed bf16 pair (v_cvt_pk_bf16_f32: round to nearest even), lo first.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const bf16x2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+  return __builtin_bit_cast(uint32_t, v);
+}
+// Two floats -> packed fp16 pair (round to nearest even), lo first.
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  const half2 v = {static_cast<_Float16>(lo), static_cast<_Float16>(hi)};
   return __builtin_bit_cast(uint32_t, v);
 }
 
@@ -105,7 +117,7 @@ __device__ __forceinline__ void sched_step() {
 #endif
 }
 
-template <int kMode>
+template <int kMode, bool kF16>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_ns_gemm(GemmArgs args) {
   constexpr bool kNN = kMode == 2;
   constexpr bool kSym = kMode != 2;
@@ -275,8 +287,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         // apply: operands swapped so each lane ends up with 4 consecutive output columns
-        if (kNN)
+        if constexpr (kNN)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+        else if constexpr (kF16)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(half8, af[i]),
+                                                              __builtin_bit_cast(half8, bfr[j]), acc[i][j], 0, 0, 0);
         else
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
       }
@@ -371,8 +386,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int out_col0 = kNN ? rowB0 : rowA0;
   float s = 1.f;
   if (g.scale_kind != 0) s = g.fold[2 * mat + (g.scale_kind - 1)];
-  const float ae = args.alpha_e * s, aa = args.alpha_acc * s;
-  const float ad = (kSym && ti == tj) ? args.alpha_diag * s : 0.f;  // diagonal tiles only
+  const float ae = g.alpha_e * s, aa = g.alpha_acc * s;
+  const float ad = (kSym && ti == tj) ? g.alpha_diag * s : 0.f;  // diagonal tiles only
   const int own_row = kNN ? wm : wn;  // 128-row half holding this wave's OUT rows
   const int own_col = kNN ? wn : wm;  // 128-column half holding this wave's OUT columns
   const int ldo = g.ldc;
@@ -411,41 +426,50 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       e[vq] = *reinterpret_cast<const lds_u32x2*>(src + stage_byte(r, c));
     }
   };
-  u32x2 ecur[4], enext[4];
-  if (kHasE) e_read(0, 0, ecur);
+  // The output format is uniform over the workgroup: one copy of the loop per format.
+  auto combine = [&](auto out16_tag) {
+    constexpr bool kOut16 = decltype(out16_tag)::value;
+    u32x2 ecur[4], enext[4];
+    if (kHasE) e_read(0, 0, ecur);
 #pragma unroll
-  for (int b = 0; b < 16; ++b) {
-    const int i = b >> 2, j = b & 3;
-    if (kHasE && b < 15) e_read((b + 1) >> 2, (b + 1) & 3, enext);
-    if (kHasE) __builtin_amdgcn_sched_barrier(0);
-    const int r = 128 * own_row + 32 * (kNN ? i : j) + (lane & 31);
+    for (int b = 0; b < 16; ++b) {
+      const int i = b >> 2, j = b & 3;
+      if (kHasE && b < 15) e_read((b + 1) >> 2, (b + 1) & 3, enext);
+      if (kHasE) __builtin_amdgcn_sched_barrier(0);
+      const int r = 128 * own_row + 32 * (kNN ? i : j) + (lane & 31);
 #pragma unroll
-    for (int vq = 0; vq < 4; ++vq) {
-      const int c = 128 * own_col + 32 * (kNN ? j : i) + 8 * vq + 4 * h;
-      float o[4];
+      for (int vq = 0; vq < 4; ++vq) {
+        const int c = 128 * own_col + 32 * (kNN ? j : i) + 8 * vq + 4 * h;
+        float o[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) o[q] = aa * acc[i][j][4 * vq + q];
+        for (int q = 0; q < 4; ++q) o[q] = aa * acc[i][j][4 * vq + q];
+        if (kHasE) {
+          const u32x2 e = ecur[vq];
+          auto up = [](uint32_t x) { return kF16 ? f16_to_f32(x) : bf16_to_f32(x); };  // E has the operands' format
+          o[0] = fmaf(ae, up(e.x & 0xffffu), o[0]);
+          o[1] = fmaf(ae, up(e.x >> 16), o[1]);
+          o[2] = fmaf(ae, up(e.y & 0xffffu), o[2]);
+          o[3] = fmaf(ae, up(e.y >> 16), o[3]);
+        }
+        if (kSym) {
+          // OUT is symmetric here, so OUT[r][c + q] is on the diagonal when r == c + q
+#pragma unroll
+          for (int q = 0; q < 4; ++q) o[q] += (r == c + q) ? ad : 0.f;
+        }
+        packed[i][j][vq].x = kOut16 ? pack_f16x2(o[0], o[1]) : pack_bf16x2(o[0], o[1]);
+        packed[i][j][vq].y = kOut16 ? pack_f16x2(o[2], o[3]) : pack_bf16x2(o[2], o[3]);
+      }
       if (kHasE) {
-        const u32x2 e = ecur[vq];
-        o[0] = fmaf(ae, bf16_to_f32(e.x & 0xffffu), o[0]);
-        o[1] = fmaf(ae, bf16_to_f32(e.x >> 16), o[1]);
-        o[2] = fmaf(ae, bf16_to_f32(e.y & 0xffffu), o[2]);
-        o[3] = fmaf(ae, bf16_to_f32(e.y >> 16), o[3]);
-      }
-      if (kSym) {
-        // OUT is symmetric here, so OUT[r][c + q] is on the diagonal when r == c + q
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] += (r == c + q) ? ad : 0.f;
+        for (int vq = 0; vq < 4; ++vq) ecur[vq] = enext[vq];
       }
-      packed[i][j][vq].x = pack_bf16x2(o[0], o[1]);
-      packed[i][j][vq].y = pack_bf16x2(o[2], o[3]);
     }
-    if (kHasE) {
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int vq = 0; vq < 4; ++vq) ecur[vq] = enext[vq];
-    }
-  }
+  };
+  if (kSym && g.out_f16)  // the X product always writes bf16
+    combine(std::true_type{});
+  else
+    combine(std::false_type{});
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -591,13 +615,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
 }  // namespace
 
-hipError_t launch_gemm(const GemmArgs& a, int mode, hipStream_t st) {
+hipError_t launch_gemm(const GemmArgs& a, int mode, int f16, hipStream_t st) {
   const int blocks = a.tile_start[a.count];
-  switch (mode) {
-    case 0: hipLaunchKernelGGL(k_ns_gemm<0>, dim3(blocks), dim3(256), 0, st, a); break;
-    case 1: hipLaunchKernelGGL(k_ns_gemm<1>, dim3(blocks), dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL(k_ns_gemm<2>, dim3(blocks), dim3(256), 0, st, a); break;
-  }
+  if (mode == 0 && f16) hipLaunchKernelGGL((k_ns_gemm<0, true>), dim3(blocks), dim3(256), 0, st, a);
+  else if (mode == 0) hipLaunchKernelGGL((k_ns_gemm<0, false>), dim3(blocks), dim3(256), 0, st, a);
+  else if (mode == 1 && f16) hipLaunchKernelGGL((k_ns_gemm<1, true>), dim3(blocks), dim3(256), 0, st, a);
+  else if (mode == 1) hipLaunchKernelGGL((k_ns_gemm<1, false>), dim3(blocks), dim3(256), 0, st, a);
+  else if (!f16) hipLaunchKernelGGL((k_ns_gemm<2, false>), dim3(blocks), dim3(256), 0, st, a);
+  else return hipErrorInvalidValue;  // the X product's operands are bf16
   return hipGetLastError();
 }
 

@@ -103,7 +103,7 @@ meq_status validate_hparams(const meq_hparams& hp) {
   if (!finite(hp.zero_rms_delta) || hp.zero_rms_delta < 0.f) return MEQ_ERR_INVALID_ARG;
   if (hp.nesterov != 0 && hp.nesterov != 1) return MEQ_ERR_INVALID_ARG;
   if (hp.update_rule != MEQ_RULE_MEQMUON && hp.update_rule != MEQ_RULE_MOONLIGHT) return MEQ_ERR_INVALID_ARG;
-  if (hp.ns_gram_steps < 1 || hp.ns_gram_steps > 2) return MEQ_ERR_INVALID_ARG;
+  if (hp.ns_gram_steps < 1 || hp.ns_gram_steps > 3) return MEQ_ERR_INVALID_ARG;
   return MEQ_OK;
 }
 
@@ -182,7 +182,7 @@ MEQ_EXPORT void meq_default_hparams(meq_hparams* hp) {
   hp->zero_rms_delta = 1e-7f;
   hp->nesterov = 0;
   hp->update_rule = MEQ_RULE_MEQMUON;
-  hp->ns_gram_steps = 2;
+  hp->ns_gram_steps = 3;
 }
 
 MEQ_EXPORT const char* meq_status_string(meq_status s) {
@@ -604,11 +604,20 @@ meq_status enqueue_prescale(meq_plan* p, char* ws, const void* const* grads, flo
 
 // Step a3 as chains of products, one chain per shape group.  Four product kinds:
 //   OP_GRAM   A <- X X^T                       (symmetric NT kernel, K = L)
-//   OP_POLY   P <- a I + b A + c A A           (symmetric NT kernel with the A tile added, K = S)
+//   OP_POLY   P <- a I + b A + c A A           (poly kernel: symmetric NT with the A tile added, K = S)
 //   OP_SPROD  C <- P M for M in {A, T, Q}      (symmetric NT kernel, K = S; P and M are commuting
 //                                               symmetric matrices, so P M = P M^T is symmetric)
 //   OP_APPLY  X' <- P X or Q X                 (NN kernel, K = S)
 enum OpKind { OP_GRAM = 0, OP_POLY = 1, OP_SPROD = 2, OP_APPLY = 3 };
+
+// Gram-space matrices are kept in fp16, whose 11-bit significand keeps the S x S iteration as
+// accurate as the printed bf16 step; A and T are stored times kGramScale so that their entries
+// (about 1/s on the diagonal of the first segment's A, and smaller off it) stay in fp16's
+// normal range.  Every entry of A and T is bounded by the largest eigenvalue, at most
+// max (phi^j(sigma))^2 <= 1.45 for A and max sigma phi(sigma) <= 1.21 for T, so the scaled
+// values stay below 1.2e4 (fp16 reaches 65504); P = p(A) and the products Q of P factors are
+// stored unscaled (eigenvalues at most a^3 < 41).
+constexpr float kGramScale = 8192.f;
 
 struct NsOp {
   int kind;
@@ -616,38 +625,48 @@ struct NsOp {
   int scale_kind;     // 2: 1/||V||^2 (first X X^T of a step), 1: 1/||V|| (first X product)
   bool rowcol;        // the step's last X product also writes the row/column sums of squares
   bool with_prev;     // independent of the previous op of the chain (may share its launch)
+  bool in_f16, out_f16;                  // operand and output formats (else bf16)
+  float alpha_acc, alpha_e, alpha_diag;  // C = alpha_acc * (product) + alpha_e * E + alpha_diag * I
 };
 
 // One shape group's products over a schedule.  A segment of j steps is eq. "ns" regrouped:
 // A = X X^T once; for each step P_i = a I + b A + c A A, then (before the segment's last
 // step) A <- P_i (P_i A), since X P-updated gives (P X)(P X)^T = P A P = P P A; the
 // segment's product Q = P_last ... P_first accumulates alongside; finally X <- Q X.  A
-// one-step segment is exactly A = X X^T, P, X <- P X.  X_0 is in buffer a when x_in_a.
+// one-step segment is exactly A = X X^T, P, X <- P X, all in bf16; a longer one keeps A, T,
+// its P factors and Q in fp16 (A and T scaled by kGramScale) and writes its last Q in bf16
+// for the X product.  X_0 is in buffer a when x_in_a.
 std::vector<NsOp> group_ops(const GroupInfo& g, const std::vector<int>& segs, bool x_in_a, bool first_fold,
-                            bool rowcol) {
+                            bool rowcol, const meq_hparams& hp) {
   std::vector<NsOp> ops;
   size_t cur = x_in_a ? g.off_xa : g.off_xb, nxt = x_in_a ? g.off_xb : g.off_xa;
   const size_t pbuf[2] = {g.off_p, g.off_p2}, qbuf[2] = {g.off_q0, g.off_q1};
   for (size_t si = 0; si < segs.size(); ++si) {
     const bool fold = first_fold && si == 0;
-    ops.push_back({OP_GRAM, cur, cur, g.off_a, 0, fold ? 2 : 0, false, false});
+    const int len = segs[si];
+    const bool f16 = len >= 2;
+    const float sc = f16 ? kGramScale : 1.f;
+    ops.push_back({OP_GRAM, cur, cur, g.off_a, 0, fold ? 2 : 0, false, false, false, f16, sc, 0.f, 0.f});
     size_t q = 0;
-    for (int j = 0; j < segs[si]; ++j) {
+    for (int j = 0; j < len; ++j) {
       const size_t pj = pbuf[j % 2];
-      ops.push_back({OP_POLY, g.off_a, g.off_a, pj, g.off_a, 0, false, false});
+      // P = a I + (b / sc) A' + (c / sc^2) A' A' for the scaled A' = sc A
+      ops.push_back({OP_POLY, g.off_a, g.off_a, pj, g.off_a, 0, false, false, f16, f16, hp.ns_c / (sc * sc),
+                     hp.ns_b / sc, hp.ns_a});
       if (j == 0) {
         q = pj;
       } else {  // Q <- P_j Q (reads the other P buffer or a Q buffer, writes the free Q buffer)
         const size_t qn = qbuf[(j - 1) % 2];
-        ops.push_back({OP_SPROD, pj, q, qn, 0, 0, false, false});
+        ops.push_back({OP_SPROD, pj, q, qn, 0, 0, false, false, true, j + 1 < len, 1.f, 0.f, 0.f});
         q = qn;
       }
-      if (j + 1 < segs[si]) {
-        ops.push_back({OP_SPROD, pj, g.off_a, g.off_t, 0, 0, false, j > 0});  // T <- P_j A
-        ops.push_back({OP_SPROD, pj, g.off_t, g.off_a, 0, 0, false, false});  // A <- P_j T
+      if (j + 1 < len) {
+        ops.push_back({OP_SPROD, pj, g.off_a, g.off_t, 0, 0, false, j > 0, true, true, 1.f, 0.f, 0.f});  // T <- P_j A
+        ops.push_back({OP_SPROD, pj, g.off_t, g.off_a, 0, 0, false, false, true, true, 1.f, 0.f, 0.f});  // A <- P_j T
       }
     }
-    ops.push_back({OP_APPLY, q, cur, nxt, 0, fold ? 1 : 0, rowcol && si + 1 == segs.size(), false});
+    ops.push_back({OP_APPLY, q, cur, nxt, 0, fold ? 1 : 0, rowcol && si + 1 == segs.size(), false, false, false,
+                   1.f, 0.f, 0.f});
     std::swap(cur, nxt);
   }
   return ops;
@@ -661,6 +680,10 @@ void fill_gemm_group(GemmGroup& gg, const NsOp& op, const GroupInfo& g, char* ws
   gg = GemmGroup{};
   gg.fold = reinterpret_cast<const float*>(ws + g.off_fold);
   gg.scale_kind = op.scale_kind;
+  gg.out_f16 = op.out_f16;
+  gg.alpha_acc = op.alpha_acc;
+  gg.alpha_e = op.alpha_e;
+  gg.alpha_diag = op.alpha_diag;
   gg.a = buf(op.a);
   gg.c = buf(op.c);
   if (op.kind == OP_APPLY) {
@@ -690,69 +713,104 @@ void fill_gemm_group(GemmGroup& gg, const NsOp& op, const GroupInfo& g, char* ws
   gg.tiles = gg.tiles_per_mat * static_cast<int>(g.mats.size());
 }
 
-// Enqueue the chains of all groups.  Launch by launch, pick the op kind with the most work
-// (tiles x K) among the chains' next ops and run every chain's next op of that kind (and the
-// ops after it that are independent of it and of the same kind) in grouped launches of up
-// to kMaxGemmGroups entries, longest K first so the long tiles start first.
+// Kernel instantiation of an op: template mode (0 symmetric NT, 1 poly, 2 apply) x operand format.
+int mode_of(const NsOp& op) { return 2 * (op.kind == OP_POLY ? 1 : op.kind == OP_APPLY ? 2 : 0) + (op.in_f16 ? 1 : 0); }
+
+// A run of a chain's ops that may share one launch: the op and the ops after it marked
+// with_prev (same kernel, independent of each other).
+struct Bundle {
+  int mode;  // kernel instantiation (mode_of): one launch runs one instantiation
+  std::vector<std::pair<int, const NsOp*>> ops;  // (shape group, op)
+};
+
+std::vector<Bundle> bundles_of(int gi, const std::vector<NsOp>& chain) {
+  std::vector<Bundle> out;
+  for (const NsOp& op : chain) {
+    const int mode = mode_of(op);
+    if (op.with_prev && !out.empty() && out.back().mode == mode)
+      out.back().ops.push_back({gi, &op});
+    else
+      out.push_back({mode, {{gi, &op}}});
+  }
+  return out;
+}
+
+// Interleave two launch sequences into a shortest common supersequence over kernel templates:
+// each output launch takes the next bundle of either sequence or, when both use the same
+// kernel, of both.  Each sequence keeps its order, and different chains are independent, so
+// every dependency is respected; equal sequences (groups on the same schedule) merge exactly.
+std::vector<Bundle> merge_launches(const std::vector<Bundle>& a, const std::vector<Bundle>& b) {
+  const size_t n = a.size(), m = b.size();
+  std::vector<std::vector<int>> len(n + 1, std::vector<int>(m + 1, 0));  // SCS length of a[i:], b[j:]
+  for (size_t i = n + 1; i-- > 0;)
+    for (size_t j = m + 1; j-- > 0;) {
+      if (i == n || j == m)
+        len[i][j] = static_cast<int>((n - i) + (m - j));
+      else if (a[i].mode == b[j].mode)
+        len[i][j] = 1 + len[i + 1][j + 1];
+      else
+        len[i][j] = 1 + std::min(len[i + 1][j], len[i][j + 1]);
+    }
+  std::vector<Bundle> out;
+  size_t i = 0, j = 0;
+  while (i < n || j < m) {
+    if (i < n && j < m && a[i].mode == b[j].mode) {
+      Bundle x = a[i++];
+      x.ops.insert(x.ops.end(), b[j].ops.begin(), b[j].ops.end());
+      ++j;
+      out.push_back(std::move(x));
+    } else if (j == m || (i < n && len[i + 1][j] <= len[i][j + 1])) {
+      out.push_back(a[i++]);
+    } else {
+      out.push_back(b[j++]);
+    }
+  }
+  return out;
+}
+
+// Enqueue the chains of all groups: the heaviest chain first, the others merged into its launch
+// sequence; each launch runs its entries in grouped launches of up to kMaxGemmGroups, longest K
+// first so the long tiles start first.
 meq_status enqueue_chains(meq_plan* p, char* ws, const std::vector<std::vector<NsOp>>& chains, hipStream_t st) {
-  const meq_hparams& hp = p->hp;
-  std::vector<size_t> head(chains.size(), 0);
-  auto work = [&](size_t gi, const NsOp& op) {
+  auto chain_work = [&](size_t gi) {
     const GroupInfo& g = p->groups[gi];
-    const double tm = static_cast<double>(g.S / kTile);
-    const double tiles = op.kind == OP_APPLY ? tm * static_cast<double>(g.L / kTile) : tm * (tm + 1) / 2;
-    return tiles * static_cast<double>(g.mats.size()) * static_cast<double>(op.kind == OP_GRAM ? g.L : g.S);
+    double w = 0.0;
+    for (const NsOp& op : chains[gi]) {
+      const double tm = static_cast<double>(g.S / kTile);
+      const double tiles = op.kind == OP_APPLY ? tm * static_cast<double>(g.L / kTile) : tm * (tm + 1) / 2;
+      w += tiles * static_cast<double>(op.kind == OP_GRAM ? g.L : g.S);
+    }
+    return w * static_cast<double>(g.mats.size());
   };
-  for (;;) {
-    double best = -1.0;
-    int kind = -1;
-    for (int k = 0; k < 4; ++k) {
-      double w = 0.0;
-      bool any = false;
-      for (size_t gi = 0; gi < chains.size(); ++gi)
-        if (head[gi] < chains[gi].size() && chains[gi][head[gi]].kind == k) {
-          w += work(gi, chains[gi][head[gi]]);
-          any = true;
-        }
-      if (any && w > best) {
-        best = w;
-        kind = k;
-      }
-    }
-    if (kind < 0) return MEQ_OK;
-    std::vector<std::pair<size_t, const NsOp*>> entries;
-    for (size_t gi = 0; gi < chains.size(); ++gi) {
-      if (head[gi] >= chains[gi].size() || chains[gi][head[gi]].kind != kind) continue;
-      entries.push_back({gi, &chains[gi][head[gi]++]});
-      while (head[gi] < chains[gi].size() && chains[gi][head[gi]].with_prev && chains[gi][head[gi]].kind == kind)
-        entries.push_back({gi, &chains[gi][head[gi]++]});
-    }
-    std::stable_sort(entries.begin(), entries.end(), [&](const auto& x, const auto& y) {
+  std::vector<int> order(chains.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int>(i);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return chain_work(x) > chain_work(y); });
+  std::vector<Bundle> seq;
+  for (int gi : order) seq = merge_launches(seq, bundles_of(gi, chains[gi]));
+  for (Bundle& launch : seq) {
+    std::stable_sort(launch.ops.begin(), launch.ops.end(), [&](const auto& x, const auto& y) {
       const GroupInfo& gx = p->groups[x.first];
       const GroupInfo& gy = p->groups[y.first];
-      return (kind == OP_GRAM ? gx.L : gx.S) > (kind == OP_GRAM ? gy.L : gy.S);
+      return (x.second->kind == OP_GRAM ? gx.L : gx.S) > (y.second->kind == OP_GRAM ? gy.L : gy.S);
     });
-    const int mode = kind == OP_POLY ? 1 : kind == OP_APPLY ? 2 : 0;
-    const int tk = kind == OP_GRAM ? MEQ_K_GRAM : kind == OP_POLY ? MEQ_K_POLY
-                 : kind == OP_APPLY ? MEQ_K_APPLY : MEQ_K_GRAM_SPACE;
-    for (size_t c0 = 0; c0 < entries.size(); c0 += kMaxGemmGroups) {
-      GemmArgs ga{};
-      ga.count = static_cast<int>(std::min<size_t>(kMaxGemmGroups, entries.size() - c0));
+    const int mode = launch.mode / 2, f16 = launch.mode % 2;
+    const int tk = mode == 0 ? MEQ_K_GRAM : mode == 1 ? MEQ_K_POLY : MEQ_K_APPLY;
+    for (size_t c0 = 0; c0 < launch.ops.size(); c0 += kMaxGemmGroups) {
       // The a X term of X <- a X + P X is carried by P: the polynomial product stores
       // a I + b A + c A A, and the X product is the plain product P X.
-      ga.alpha_e = kind == OP_POLY ? hp.ns_b : 0.f;
-      ga.alpha_acc = kind == OP_POLY ? hp.ns_c : 1.f;
-      ga.alpha_diag = kind == OP_POLY ? hp.ns_a : 0.f;
+      GemmArgs ga{};
+      ga.count = static_cast<int>(std::min<size_t>(kMaxGemmGroups, launch.ops.size() - c0));
       int start = 0;
       for (int q = 0; q < ga.count; ++q) {
-        fill_gemm_group(ga.grp[q], *entries[c0 + q].second, p->groups[entries[c0 + q].first], ws);
+        fill_gemm_group(ga.grp[q], *launch.ops[c0 + q].second, p->groups[launch.ops[c0 + q].first], ws);
         ga.tile_start[q] = start;
         start += (ga.grp[q].tiles + 7) / 8 * 8;
       }
       ga.tile_start[ga.count] = start;
-      MEQ_TRY(timed_launch(p, tk, st, [&] { return launch_gemm(ga, mode, st); }));
+      MEQ_TRY(timed_launch(p, tk, st, [&] { return launch_gemm(ga, mode, f16, st); }));
     }
   }
+  return MEQ_OK;
 }
 
 // Step a3 of a full step: every group over its own schedule, X_0 in buffer a, the prescale
@@ -760,7 +818,7 @@ meq_status enqueue_chains(meq_plan* p, char* ws, const std::vector<std::vector<N
 // sums of squares of its output (step a4's partials).
 meq_status enqueue_ns(meq_plan* p, char* ws, bool rowcol, hipStream_t st) {
   std::vector<std::vector<NsOp>> chains;
-  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, g.segs, true, true, rowcol));
+  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, g.segs, true, true, rowcol, p->hp));
   return enqueue_chains(p, ws, chains, st);
 }
 
@@ -768,7 +826,7 @@ meq_status enqueue_ns(meq_plan* p, char* ws, bool rowcol, hipStream_t st) {
 // one): iteration k reads buffer a when k is even.
 meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, hipStream_t st) {
   std::vector<std::vector<NsOp>> chains;
-  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, {1}, k % 2 == 0, k == 0, false));
+  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, {1}, k % 2 == 0, k == 0, false, p->hp));
   return enqueue_chains(p, ws, chains, st);
 }
 

@@ -56,8 +56,9 @@ struct NormArgs {
 };
 
 // ------------------------------------------------------------------------ NS GEMMs
-// C = s * (alpha_e * E + alpha_acc * (Aop . Bop) + alpha_diag * I) stored as bf16, batched over the
-// matrices of a shape group; one launch covers up to kMaxGemmGroups groups.  Aop is
+// C = s * (alpha_e * E + alpha_acc * (Aop . Bop) + alpha_diag * I) stored as bf16 or fp16, batched over
+// the matrices of a shape group; one launch covers up to kMaxGemmGroups groups.  The operands
+// (and E) are bf16 or, for the Gram-space products, fp16 (one format per launch).  Aop is
 // M x K row-major.  Bop is N x K row-major (NT) or K x N row-major (NN).  For the
 // symmetric products only tiles on or above the diagonal are computed and each
 // off-diagonal tile is also stored mirrored: Aop . Bop^T must be symmetric (X X^T, or
@@ -77,6 +78,8 @@ struct GemmGroup {
   int tiles;           // batch * tiles_per_mat
   int scale_kind;      // 0 none, 1 scale by 1/||V||, 2 scale by 1/||V||^2 (first products of a step)
   int symmetrize;      // symmetric products of two different factors: make diagonal tiles exactly symmetric
+  int out_f16;         // store C as fp16 (Gram-space matrices) instead of bf16
+  float alpha_e, alpha_acc, alpha_diag;  // alpha_diag: symmetric products only
   // apply product only, when not null: sums of squares of the bf16 output per row of each
   // 256-column tile (rpart, (L/256) x S per matrix) and per column of each 256-row tile
   // (cpart, (S/256) x L per matrix), the partials of eq. "row-col-rms" for the last iteration
@@ -87,8 +90,6 @@ struct GemmGroup {
 
 struct GemmArgs {
   int count;                             // groups in this launch
-  float alpha_e, alpha_acc;
-  float alpha_diag;                      // symmetric products only
   int tile_start[kMaxGemmGroups + 1];    // workgroup ranges per group, multiples of 8
   GemmGroup grp[kMaxGemmGroups];
 };
@@ -171,7 +172,8 @@ struct VecArgs {
 // Launchers (defined in the .hip files).  Each returns the hipError_t of the launch.
 hipError_t launch_momentum(const MomentumArgs& a, int grad_bf16, int total_tiles, hipStream_t st);
 hipError_t launch_norm(const NormArgs& a, hipStream_t st);
-hipError_t launch_gemm(const GemmArgs& a, int mode, hipStream_t st);  // 0 Gram, 1 poly, 2 apply
+// mode 0 symmetric NT, 1 poly, 2 apply; f16: fp16 operands (modes 0 and 1)
+hipError_t launch_gemm(const GemmArgs& a, int mode, int f16, hipStream_t st);
 hipError_t launch_rowcol(const RowColArgs& a, int batch, hipStream_t st);
 hipError_t launch_rms(const SelectArgs& a, hipStream_t st);
 hipError_t launch_select(const SelectArgs& a, hipStream_t st);

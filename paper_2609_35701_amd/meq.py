@@ -20,9 +20,9 @@ PARAM_HIDDEN, PARAM_AUX, PARAM_VECTOR = 0, 1, 2
 RULE_MEQMUON, RULE_MOONLIGHT = 0, 1
 BUF_X0, BUF_U, BUF_NORMSQ, BUF_ROW_RMS, BUF_COL_RMS, BUF_SCALE = range(6)
 (K_MOMENTUM, K_NORM, K_GRAM, K_POLY, K_APPLY, K_ROWCOL, K_SELECT, K_UPDATE,
- K_AUX_ROWS, K_AUX_COLS, K_AUX_UPDATE, K_VECTOR, K_GRAM_SPACE) = range(13)
+ K_AUX_ROWS, K_AUX_COLS, K_AUX_UPDATE, K_VECTOR) = range(12)
 KERNEL_NAMES = ("momentum", "norm", "gram", "poly", "apply", "rowcol", "select", "update",
-                "aux_rows", "aux_cols", "aux_update", "vector", "gram_space")
+                "aux_rows", "aux_cols", "aux_update", "vector")
 
 EXPORTED = ("meq_default_hparams", "meq_init", "meq_init_kind", "meq_workspace_bytes", "meq_step",
             "meq_get_stats", "meq_ns_cv_trace", "meq_destroy", "meq_status_string", "meq_plan_num_groups", "meq_plan_group",

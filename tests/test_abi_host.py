@@ -29,7 +29,7 @@ def test_library_exports_every_header_symbol():
 
 def test_default_hparams_are_the_papers():
     hp = meq.default_hparams()
-    assert hp.ns_steps == 5 and hp.nesterov == 0 and hp.ns_gram_steps == 2
+    assert hp.ns_steps == 5 and hp.nesterov == 0 and hp.ns_gram_steps == 3
     for got, want in [(hp.mu, 0.95), (hp.rho, 0.2), (hp.weight_decay, 0.1), (hp.ns_a, 3.4445),
                       (hp.ns_b, -4.7750), (hp.ns_c, 2.0315), (hp.zero_rms_delta, 1e-7)]:
         assert got == pytest.approx(want, rel=1e-6)
@@ -73,7 +73,7 @@ def test_init_validates_descriptors(desc, status):
 @pytest.mark.parametrize("field,value", [("mu", 1.0), ("mu", -0.1), ("mu", float("nan")), ("rho", 0.0),
                                          ("weight_decay", -1.0), ("ns_steps", 0), ("ns_steps", 65),
                                          ("ns_a", float("inf")), ("zero_rms_delta", -1e-7), ("nesterov", 2),
-                                         ("ns_gram_steps", 0), ("ns_gram_steps", 3)])
+                                         ("ns_gram_steps", 0), ("ns_gram_steps", 4)])
 def test_init_validates_hparams(field, value):
     hp = meq.default_hparams(**{field: value})
     assert _init([(4, 8, meq.MEQ_BF16, meq.MEQ_BF16)], hp) == meq.MEQ_ERR_INVALID_ARG
@@ -105,18 +105,19 @@ def test_grouping_of_the_1b_shapes():
 
 
 @pytest.mark.parametrize("shape,steps,gram,segs", [
-    ((256, 512), 5, 2, [2, 2, 1]),       # padded long side 2x the short side: Gram-space segments
-    ((512, 256), 5, 2, [2, 2, 1]),       # tall matrices run in wide orientation
-    ((512, 512), 5, 2, [1] * 5),         # square: eq. "ns" as printed
-    ((256, 300), 5, 2, [2, 2, 1]),       # the padded sizes decide: 256 x 512
-    ((256, 257), 5, 2, [2, 2, 1]),
-    ((2048, 3840), 5, 2, [1] * 5),       # 1.875x: not worth it
+    ((256, 512), 5, 3, [3, 2]),          # padded long side 2x the short side: Gram-space segments
+    ((512, 256), 5, 3, [3, 2]),          # tall matrices run in wide orientation
+    ((512, 512), 5, 3, [1] * 5),         # square: eq. "ns" as printed
+    ((256, 300), 5, 3, [3, 2]),          # the padded sizes decide: 256 x 512
+    ((256, 257), 5, 3, [3, 2]),
+    ((2048, 3840), 5, 3, [1] * 5),       # 1.875x: not worth it
     ((2048, 8192), 5, 1, [1] * 5),       # ns_gram_steps 1: the printed iteration everywhere
-    ((2048, 8192), 4, 2, [2, 2]),
-    ((2048, 8192), 3, 2, [2, 1]),
-    ((2048, 8192), 7, 2, [2, 2, 2, 1]),
-    ((2048, 8192), 2, 2, [2]),
-    ((1, 300), 1, 2, [1]),
+    ((2048, 8192), 5, 2, [2, 2, 1]),
+    ((2048, 8192), 4, 3, [3, 1]),
+    ((2048, 8192), 3, 3, [3]),
+    ((2048, 8192), 7, 3, [3, 3, 1]),
+    ((2048, 8192), 2, 3, [2]),
+    ((1, 300), 1, 3, [1]),
 ])
 def test_newton_schulz_schedule(shape, steps, gram, segs):
     plan = meq.Plan([shape], "bf16", hparams=meq.default_hparams(ns_steps=steps, ns_gram_steps=gram))
@@ -129,11 +130,11 @@ def test_schedule_of_the_1b_shapes_and_workspace():
     shapes = [(m.rows, m.cols) for m in wl.matrices]
     plan = meq.Plan(shapes, "bf16")
     sched = {plan.groups()[g][:2]: plan.schedule(g) for g in range(len(plan.groups()))}
-    assert sched == {(2048, 2048): [1] * 5, (512, 2048): [2, 2, 1], (2048, 8192): [2, 2, 1]}
+    assert sched == {(2048, 2048): [1] * 5, (512, 2048): [3, 2], (2048, 8192): [3, 2]}
     literal = meq.Plan(shapes, "bf16", hparams=meq.default_hparams(ns_gram_steps=1))
     assert all(literal.schedule(g) == [1] * 5 for g in range(3))
-    # three more s x s bf16 buffers per matrix of the two segmented groups (P', T, Q)
-    extra = 3 * 2 * (48 * 2048 * 2048 + 32 * 512 * 512)
+    # four more s x s 16-bit buffers per matrix of the two segmented groups (P', T, Q, Q')
+    extra = 4 * 2 * (48 * 2048 * 2048 + 32 * 512 * 512)
     assert plan.workspace_bytes - literal.workspace_bytes == pytest.approx(extra, abs=64 * 256)
     L = meq.lib()
     n = ctypes.c_int32()
@@ -173,8 +174,8 @@ def test_debug_regions_and_timing_kinds():
     off_x0, r, c, ld = plan.debug_region(0, meq.BUF_X0)
     assert (r, c, ld) == (100, 300, 512)  # wide orientation, long side padded to 256
     off_u, *_ = plan.debug_region(0, meq.BUF_U)
-    assert plan.schedule(0) == [2, 2, 1]
-    assert off_u != off_x0  # three segments: the output is in the second buffer
+    assert plan.schedule(0) == [3, 2]
+    assert off_u == off_x0  # two segments: the second one writes back into the first buffer
     off_x0, *_ = plan.debug_region(1, meq.BUF_X0)
     off_u, *_ = plan.debug_region(1, meq.BUF_U)
     assert plan.schedule(1) == [1] * 5

@@ -50,11 +50,11 @@ def test_one_ns_step_keeps_x0(dtype):
     run_and_check(wl, [0, 1, 2], steps=2, hp=meq.default_hparams(ns_steps=1), label=wl.name)
 
 
-@pytest.mark.parametrize("steps,gram", [(5, 1), (4, 2), (3, 2), (7, 2), (2, 2), (1, 2)])
+@pytest.mark.parametrize("steps,gram", [(5, 1), (5, 2), (4, 3), (3, 3), (7, 3), (2, 3), (1, 3)])
 def test_newton_schulz_schedules(steps, gram):
-    """Schedules other than the default 2 + 2 + 1 (eq. "ns" as printed; 2 + 2, 2 + 1,
-    2 + 2 + 2 + 1 and single segments of 2 and 1 steps) against the printed iteration in fp64;
-    X_0 is checked bit for bit when a schedule has one segment."""
+    """Schedules other than the default 3 + 2 (eq. "ns" as printed; 2 + 2 + 1, 3 + 1, one
+    segment of 3, 3 + 3 + 1, one segment of 2 and a single step) against the printed iteration in
+    fp64; X_0 is checked bit for bit when a schedule has one segment."""
     wl = workloads.custom([(256, 768), (1376, 512), (300, 100), (512, 512)], "bf16", name=f"sched-{steps}-{gram}")
     hp = meq.default_hparams(ns_steps=steps, ns_gram_steps=gram)
     run, _ = run_and_check(wl, range(4), steps=2, hp=hp, label=f"schedule K={steps} g={gram}")
@@ -193,11 +193,11 @@ def test_timing_events_report_every_kernel():
     log("[case] timing")
     wl = workloads.custom([(512, 2048), (2048, 512)], "bf16", name="timing")
     run = Run(wl, [0, 1])
-    hidden_kinds = list(range(8)) + [meq.K_GRAM_SPACE]
+    hidden_kinds = list(range(8))
     run.upd.plan.set_timing(hidden_kinds)
     run.step(LR)
     segs = run.upd.plan.schedule(0)
-    assert segs == [2, 2, 1]
+    assert segs == [3, 2]
     for kind in hidden_kinds:
         ms, n = run.upd.plan.get_timing(kind)
         if kind == meq.K_ROWCOL:
@@ -207,13 +207,12 @@ def test_timing_events_report_every_kernel():
         assert n >= 1 and ms > 0, meq.KERNEL_NAMES[kind]
     ms, n = run.upd.plan.get_timing(meq.K_APPLY)
     assert n == len(segs)  # one X product per segment for the single shape group
-    ms, n = run.upd.plan.get_timing(meq.K_GRAM)
-    assert n == len(segs)
     ms, n = run.upd.plan.get_timing(meq.K_POLY)
     assert n == 5
-    ms, n = run.upd.plan.get_timing(meq.K_GRAM_SPACE, reset=True)
-    # each 2-step segment: P A and P T at its first step, P Q at its second
-    assert n == 6
+    ms, n = run.upd.plan.get_timing(meq.K_GRAM, reset=True)
+    # X X^T once per segment; P A and P T at every step but a segment's last, P Q at every step
+    # but a segment's first (sharing its launch with P A where both run)
+    assert n == len(segs) + 5 + 3
     assert run.upd.plan.get_timing(meq.K_APPLY) == (0.0, 0)
     # the row/column sums kernel of its own still runs in the CV trace (no apply before X_0)
     run.upd.plan.set_timing([meq.K_ROWCOL])
