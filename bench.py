@@ -27,6 +27,11 @@ GEMM_SOURCE = os.path.join(ROOT, "paper_2609_35701_amd", "csrc", "k_ns_gemm.hip"
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "k_ns_gemm_apply_llama1b_traffic.md")
 CALIBRATION_BYTES = 256 << 20  # the plain copy kernel of known size: 256 MiB read + 256 MiB written
 CALIBRATION_KERNEL = "neg_kernel"  # torch.neg on fp32 is the copy (one read, one write per element)
+# Kernel instantiations of the NS products: template mode (0 symmetric NT, 1 poly, 2 apply) and
+# operand format (fp16 for the Gram-space products).
+APPLY_KERNEL = "k_ns_gemm<2, false>"
+NS_KERNELS = ("k_ns_gemm<0, false>", "k_ns_gemm<0, true>", "k_ns_gemm<1, false>", "k_ns_gemm<1, true>",
+              APPLY_KERNEL)
 
 
 def gemm_source_hash() -> str:
@@ -90,7 +95,7 @@ def summarize_traffic(fetch_dir: str, write_dir: str, out: str, fetch_cmd: str, 
         f_kib, n = fe.get(k, (float("nan"), 0))
         w_kib, _ = wr.get(k, (float("nan"), 0))
         rows.append((k, n, f_kib, w_kib, f_kib * 1024 / cf + w_kib * 1024 / cw))
-    apply = [r for r in rows if r[0] == "k_ns_gemm<2>"][0]
+    apply = [r for r in rows if r[0] == APPLY_KERNEL][0]
     lines = [
         "# HBM traffic per dispatch (rocprofv3 FETCH_SIZE / WRITE_SIZE), llama-1b step\n\n",
         "Commands (from the repository root on one MI355X; each counter in a run of its own):\n\n",
@@ -106,7 +111,7 @@ def summarize_traffic(fetch_dir: str, write_dir: str, out: str, fetch_cmd: str, 
     for k, n, f_kib, w_kib, b in rows:
         lines.append(f"| {k} | {n} | {f_kib:.0f} | {w_kib:.0f} | {b:.4g} |\n")
     lines += [
-        "\nRecorded for the benchmark's roofline (apply product, k_ns_gemm<2>):\n\n",
+        f"\nRecorded for the benchmark's roofline (apply product, {APPLY_KERNEL}):\n\n",
         f"- traffic_bytes_per_launch: {apply[4]:.6g}\n",
         f"- kernel_source_sha256: {gemm_source_hash()}\n",
     ]
@@ -114,7 +119,7 @@ def summarize_traffic(fetch_dir: str, write_dir: str, out: str, fetch_cmd: str, 
         f.write("".join(lines))
 
 
-def timed_region_average(trace_csv: str, line: dict, kernel: str = "k_ns_gemm<2>") -> tuple:
+def timed_region_average(trace_csv: str, line: dict, kernel: str = APPLY_KERNEL) -> tuple:
     """Average duration (ms) and count of `kernel`'s dispatches inside the benchmark's timed region,
     from a rocprofv3 kernel trace of the same run: the main plan runs warmup + steps steps first,
     with roofline.launches_per_step launches of the kernel each; later legs follow them."""
@@ -152,7 +157,7 @@ def summarize_stats(stats_csv: str, out: str, command: str, note: str, trace_csv
             f"Timed region of the same run (summarised with `python bench.py --summarize-stats <stats csv> "
             f"--trace <trace csv> --bench-json <bench line> --out <this file>`): {line['steps']} steps after "
             f"{line['warmup']} warm-up steps, {line['ms_per_step']:.3f} ms/step under the profiler; the apply "
-            f"product k_ns_gemm<2> launches {line['roofline']['launches_per_step']:g} times per step. Its "
+            f"product {APPLY_KERNEL} launches {line['roofline']['launches_per_step']:g} times per step. Its "
             f"average over the {n} timed-region dispatches in the rocprofv3 trace is {avg:.4f} ms; the "
             f"bench line reports {line['roofline']['avg_launch_ms']:.4f} ms from HIP events on its launch "
             "stream. The table below averages every dispatch of the run, including the legs after the "
@@ -168,32 +173,38 @@ def summarize_stats(stats_csv: str, out: str, command: str, note: str, trace_csv
         f.write("".join(lines))
 
 
-MFMA_COUNTERS = ("GRBM_GUI_ACTIVE", "SQ_BUSY_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+MFMA_COUNTERS = ("GRBM_GUI_ACTIVE", "SQ_BUSY_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16",
+                 "SQ_INSTS_VALU_MFMA_MOPS_F16")
 SIMDS = 256 * 4  # MI355X: 256 compute units of 4 SIMDs
 XCDS = 8
 
 
 def ns_launch_flops(wl) -> dict:
-    """Per step, for each NS kernel template over all shape groups: (algorithmic symmetric-aware
+    """Per step, for each NS kernel instantiation over all shape groups: (algorithmic symmetric-aware
     flops, flops the 256 x 256 tiles execute, padding and the lower half of diagonal tiles
-    included), under the default schedule of each shape group."""
+    included), under the default schedule of each shape group: X X^T runs in k_ns_gemm<0, false>,
+    the Gram-space products of multi-step segments in k_ns_gemm<0, true>, the polynomial of a
+    one-step segment in k_ns_gemm<1, false> and of a longer one in k_ns_gemm<1, true>."""
     from paper_2609_35701_amd import meq
 
     plan = meq.Plan([(m.rows, m.cols) for m in wl.matrices], wl.param_dtype)
     segs = {(s, l): plan.schedule(g) for g, (s, l, _) in enumerate(plan.groups())}
-    out = {"k_ns_gemm<0>": [0, 0], "k_ns_gemm<1>": [0, 0], "k_ns_gemm<2>": [0, 0]}
+    out = {k: [0, 0] for k in NS_KERNELS}
     for m in wl.matrices:
         s, l = min(m.rows, m.cols), max(m.rows, m.cols)
         sp, lp = -(-s // 256) * 256, -(-l // 256) * 256
         tm, tl = sp // 256, lp // 256
         tri = tm * (tm + 1) // 2
         sg = segs[(s, l)]
-        nseg, steps = len(sg), sum(sg)
+        nseg = len(sg)
         nsprod = sum(3 * (j - 1) for j in sg)
-        for k, alg, exe in (("k_ns_gemm<0>", nseg * s * s * l + nsprod * s ** 3,
-                             nseg * tri * 2 * 256 * 256 * lp + nsprod * tri * 2 * 256 * 256 * sp),
-                            ("k_ns_gemm<1>", steps * s ** 3, steps * tri * 2 * 256 * 256 * sp),
-                            ("k_ns_gemm<2>", nseg * 2 * s * s * l, nseg * tm * tl * 2 * 256 * 256 * sp)):
+        poly16 = sum(j for j in sg if j > 1)
+        poly_bf = sum(j for j in sg if j == 1)
+        for k, alg, exe in (("k_ns_gemm<0, false>", nseg * s * s * l, nseg * tri * 2 * 256 * 256 * lp),
+                            ("k_ns_gemm<0, true>", nsprod * s ** 3, nsprod * tri * 2 * 256 * 256 * sp),
+                            ("k_ns_gemm<1, false>", poly_bf * s ** 3, poly_bf * tri * 2 * 256 * 256 * sp),
+                            ("k_ns_gemm<1, true>", poly16 * s ** 3, poly16 * tri * 2 * 256 * 256 * sp),
+                            (APPLY_KERNEL, nseg * 2 * s * s * l, nseg * tm * tl * 2 * 256 * 256 * sp)):
             out[k][0] += alg
             out[k][1] += exe
     return out
@@ -219,20 +230,24 @@ def summarize_mfma(run_dir: str, out: str, command: str, workload: str, note: st
         f"Per step ({steps} meq_step calls in the run, warm-up included): GRBM_GUI_ACTIVE summed over the 8 XCDs "
         f"(divided by 8: cycles the kernel template was active); SQ_VALU_MFMA_BUSY_CYCLES summed over all {SIMDS} "
         f"SIMDs (divided by {SIMDS} and by the active cycles: fraction of the time a SIMD's matrix core was busy); "
-        "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 = bf16 flops the matrix cores executed, against the flops the "
+        "SQ_INSTS_VALU_MFMA_MOPS_BF16 (SQ_INSTS_VALU_MFMA_MOPS_F16 for the fp16 instantiations) x 512 = flops "
+        "the matrix cores executed, against the flops the "
         "256 x 256 tiles execute by count (padding and the lower half of diagonal tiles of the symmetric "
         "products included) and the algorithmic symmetric-aware flops of the step's schedule. "
-        "k_ns_gemm<0> covers both X X^T and the Gram-space products P A, P T, P Q.\n\n",
+        "k_ns_gemm<0, false> runs X X^T, k_ns_gemm<0, true> the fp16 Gram-space products P A, P T, P Q, "
+        "k_ns_gemm<1, *> the polynomial of one-step (bf16) and longer (fp16) segments, "
+        "k_ns_gemm<2, false> the X products.\n\n",
         (note + "\n\n" if note else ""),
         "| kernel | dispatches per step | active cycles per step | MFMA busy | MOPS x 512 per step | tile flops "
         "per step | algorithmic flops per step | MOPS x 512 / tile flops |\n",
         "|---|---|---|---|---|---|---|---|\n",
     ]
-    for k in ("k_ns_gemm<0>", "k_ns_gemm<1>", "k_ns_gemm<2>"):
+    for k in NS_KERNELS:
         gui, n = tot["GRBM_GUI_ACTIVE"].get(k, (float("nan"), 0))
         cyc = gui / XCDS / steps
         busy = tot["SQ_VALU_MFMA_BUSY_CYCLES"].get(k, (float("nan"), 0))[0] / SIMDS / steps / cyc
-        mops = tot["SQ_INSTS_VALU_MFMA_MOPS_BF16"].get(k, (float("nan"), 0))[0] * 512 / steps
+        ctr = "SQ_INSTS_VALU_MFMA_MOPS_F16" if k.endswith("true>") else "SQ_INSTS_VALU_MFMA_MOPS_BF16"
+        mops = tot[ctr].get(k, (float("nan"), 0))[0] * 512 / steps
         alg, exe = flops[k]
         lines.append(f"| {k} | {n / steps:.4g} | {cyc:.4g} | {busy:.1%} | {mops:.4g} | {exe:.4g} | {alg:.4g} | "
                      f"{mops / exe:.4f} |\n")
@@ -550,13 +565,13 @@ def main() -> int:
             fl[k] = fl.get(k, 0) + v
     pbytes = 2 if wl.param_dtype == "bf16" else 4
     sb = stage_bytes(wl.elements, pbytes, kern["rowcol"]["launches_per_step"] > 0)
-    # kernel templates: k_ns_gemm<0> runs X X^T and the Gram-space products ("gram" timing kind)
+    # timing kinds by kernel template: k_ns_gemm<0, *> runs X X^T and the Gram-space products ("gram")
     kflops = {"gram": fl["gram"] + fl["gram_space"], "poly": fl["poly"], "apply": fl["apply"]}
     ns_kinds = ("gram", "poly", "apply")
     ns_ms = sum(kern[k]["ms_per_step"] for k in ns_kinds)
     ap_ms = kern["apply"]["ms_per_step"]
     apply_tflops = fl["apply"] / (ap_ms * 1e-3) / 1e12
-    roofline = {"bound": "mfma", "kernel": "k_ns_gemm<2> (X <- P X, or Q X after a Gram-space segment; bf16 MFMA)",
+    roofline = {"bound": "mfma", "kernel": f"{APPLY_KERNEL} (X <- P X, or Q X after a Gram-space segment; bf16 MFMA)",
                 "achieved": apply_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": apply_tflops / PEAK_BF16_TFLOPS, "traffic": recorded_traffic(wl.name),
                 "flops_per_launch": fl["apply"] / max(kern["apply"]["launches_per_step"], 1),
