@@ -84,20 +84,21 @@ typedef enum { MEQ_RULE_MEQMUON = 0, MEQ_RULE_MOONLIGHT = 1 } meq_update_rule;
  *   update_rule    meq_update_rule; MEQ_RULE_MOONLIGHT only for MEQ_PARAM_HIDDEN plans
  *   ns_gram_steps  g, 1 <= g <= 3: the most Newton-Schulz steps one Gram-space segment
  *                  covers.  g = 1 runs eq. "ns" as printed: every step forms A = X X^T,
- *                  the polynomial P = a I + b A + c A A and X <- P X (bf16 operands,
- *                  fp32 accumulation).  With g >= 2, a matrix whose padded long side is
- *                  at least twice its padded short side runs its K steps in segments of at
- *                  most g steps: a segment forms A = X X^T once, then iterates on s x s
- *                  matrices only (each step's P is a polynomial of A, so
- *                  A_{k+1} = P_k A_k P_k and the segment's product Q = P_last ... P_first
- *                  are symmetric and commute), and ends with one product X <- Q X.  The
- *                  s x s matrices of a segment are held in fp16 (A scaled by 2^13), whose
- *                  11-bit significand keeps the regrouped iteration at least as accurate as
- *                  the printed bf16 step; X and the final Q are bf16.  Equal to eq. "ns" in
- *                  exact arithmetic; it replaces most s x l products by s x s ones.
- *                  Segments are g steps long, the last one takes the remainder (K = 5,
- *                  g = 3: 3 + 2).  Default 3.  Longer segments are not offered: a single
- *                  segment of 4 or 5 steps loses accuracy on rank-deficient inputs.
+ *                  the polynomial P = a I + b A + c A A and X <- P X.  With g >= 2, a
+ *                  matrix whose padded long side is at least twice its padded short side
+ *                  runs its K steps in segments of at most g steps: a segment forms
+ *                  A = X X^T once, then iterates on s x s matrices only (each step's P is a
+ *                  polynomial of A, so A_{k+1} = P_k A_k P_k and the segment's product
+ *                  Q = P_last ... P_first are symmetric and commute), and ends with one
+ *                  product X <- Q X.  Equal to eq. "ns" in exact arithmetic; it replaces
+ *                  most s x l products by s x s ones.  Segments are g steps long, the last
+ *                  one takes the remainder (K = 5, g = 3: 3 + 2).  Default 3.  Longer
+ *                  segments are not offered: a single segment of 4 or 5 steps loses
+ *                  accuracy on rank-deficient inputs.
+ *                  Precision in every schedule: fp32 accumulation; X and the matrix that
+ *                  multiplies it (P of a printed step, a segment's final Q) in bf16; A = X X^T
+ *                  and the other s x s matrices of a segment in fp16 (A scaled by 2^13), whose
+ *                  11-bit significand keeps the iteration more accurate than bf16 storage.
  * ns_steps, ns_a/b/c and ns_gram_steps only matter for hidden plans but are validated for
  * every plan.
  */

@@ -610,10 +610,10 @@ meq_status enqueue_prescale(meq_plan* p, char* ws, const void* const* grads, flo
 //   OP_APPLY  X' <- P X or Q X                 (NN kernel, K = S)
 enum OpKind { OP_GRAM = 0, OP_POLY = 1, OP_SPROD = 2, OP_APPLY = 3 };
 
-// Gram-space matrices are kept in fp16, whose 11-bit significand keeps the S x S iteration as
-// accurate as the printed bf16 step; A and T are stored times kGramScale so that their entries
-// (about 1/s on the diagonal of the first segment's A, and smaller off it) stay in fp16's
-// normal range.  Every entry of A and T is bounded by the largest eigenvalue, at most
+// Gram matrices A = X X^T and the Gram-space matrices are kept in fp16, whose 11-bit
+// significand keeps the S x S iteration more accurate than the printed bf16 step; A and T are
+// stored times kGramScale so that their entries (about 1/s on the diagonal of the first A, and
+// smaller off it) stay in fp16's normal range.  Every entry of A and T is bounded by the largest eigenvalue, at most
 // max (phi^j(sigma))^2 <= 1.45 for A and max sigma phi(sigma) <= 1.21 for T, so the scaled
 // values stay below 1.2e4 (fp16 reaches 65504); P = p(A) and the products Q of P factors are
 // stored unscaled (eigenvalues at most a^3 < 41).
@@ -633,9 +633,10 @@ struct NsOp {
 // A = X X^T once; for each step P_i = a I + b A + c A A, then (before the segment's last
 // step) A <- P_i (P_i A), since X P-updated gives (P X)(P X)^T = P A P = P P A; the
 // segment's product Q = P_last ... P_first accumulates alongside; finally X <- Q X.  A
-// one-step segment is exactly A = X X^T, P, X <- P X, all in bf16; a longer one keeps A, T,
-// its P factors and Q in fp16 (A and T scaled by kGramScale) and writes its last Q in bf16
-// for the X product.  X_0 is in buffer a when x_in_a.
+// one-step segment is exactly A = X X^T, P, X <- P X.  A is always fp16 (scaled by
+// kGramScale); a longer segment also keeps T, its P factors and Q in fp16; the matrix that
+// feeds the X product (P of a one-step segment, the last Q of a longer one) is bf16, like X.
+// X_0 is in buffer a when x_in_a.
 std::vector<NsOp> group_ops(const GroupInfo& g, const std::vector<int>& segs, bool x_in_a, bool first_fold,
                             bool rowcol, const meq_hparams& hp) {
   std::vector<NsOp> ops;
@@ -644,14 +645,14 @@ std::vector<NsOp> group_ops(const GroupInfo& g, const std::vector<int>& segs, bo
   for (size_t si = 0; si < segs.size(); ++si) {
     const bool fold = first_fold && si == 0;
     const int len = segs[si];
-    const bool f16 = len >= 2;
-    const float sc = f16 ? kGramScale : 1.f;
-    ops.push_back({OP_GRAM, cur, cur, g.off_a, 0, fold ? 2 : 0, false, false, false, f16, sc, 0.f, 0.f});
+    const bool f16 = len >= 2;  // P factors in fp16 (they feed fp16 products, not the X product)
+    const float sc = kGramScale;
+    ops.push_back({OP_GRAM, cur, cur, g.off_a, 0, fold ? 2 : 0, false, false, false, true, sc, 0.f, 0.f});
     size_t q = 0;
     for (int j = 0; j < len; ++j) {
       const size_t pj = pbuf[j % 2];
       // P = a I + (b / sc) A' + (c / sc^2) A' A' for the scaled A' = sc A
-      ops.push_back({OP_POLY, g.off_a, g.off_a, pj, g.off_a, 0, false, false, f16, f16, hp.ns_c / (sc * sc),
+      ops.push_back({OP_POLY, g.off_a, g.off_a, pj, g.off_a, 0, false, false, true, f16, hp.ns_c / (sc * sc),
                      hp.ns_b / sc, hp.ns_a});
       if (j == 0) {
         q = pj;
