@@ -99,6 +99,12 @@ typedef enum { MEQ_RULE_MEQMUON = 0, MEQ_RULE_MOONLIGHT = 1 } meq_update_rule;
  *                  multiplies it (P of a printed step, a segment's final Q) in bf16; A = X X^T
  *                  and the other s x s matrices of a segment in fp16 (A scaled by 2^13), whose
  *                  11-bit significand keeps the iteration more accurate than bf16 storage.
+ *                  fp16 needs bounded iterates: meq_init bounds the singular values of 64
+ *                  steps of the plan's coefficients (each step maps [0, r] into
+ *                  [0, max |a x + b x^3 + c x^5| on [0, r]]) and, unless the scaled matrices
+ *                  stay below 16384, runs every matrix through the printed iteration with all
+ *                  matrices in bf16 (segments are then not used).  The paper's coefficients
+ *                  keep every singular value below 1.21 and pass.
  * ns_steps, ns_a/b/c and ns_gram_steps only matter for hidden plans but are validated for
  * every plan.
  */

@@ -53,6 +53,43 @@ struct GroupInfo {
   int64_t stride_x, stride_a, stride_rpart, stride_cpart;  // elements per matrix
 };
 
+// Gram matrices A = X X^T and the Gram-space matrices are kept in fp16, whose 11-bit
+// significand keeps the S x S iteration more accurate than the printed bf16 step; A and T are
+// stored times kGramScale so that their entries (about 1/s on the diagonal of the first A, and
+// smaller off it) stay in fp16's normal range.
+constexpr float kGramScale = 8192.f;
+
+// Whether fp16 storage is safe for the plan's coefficients.  X_0 = V/||V||_F has singular values
+// in [0, 1], and a step maps [0, r] into [0, max |phi| on [0, r]] (phi(x) = a x + b x^3 + c x^5),
+// so r_k bounds the singular values of X_k.  Every entry of a symmetric matrix is bounded by its
+// largest eigenvalue: A_k by r_k^2, T = P A by max |p(l) l| and P = p(A) by max |p(l)| for
+// l in [0, r_k^2] (p(l) = a + b l + c l^2), and a segment's Q by max |p|^3.  The bounds are taken
+// over 64 steps (the CV trace's limit) by dense sampling with 2% slack, and fp16 (65504 at most)
+// is used when the scaled values stay below 16384.  The paper's coefficients give r <= 1.21:
+// A * kGramScale <= 1.21e4, T * kGramScale <= 1.0e4, Q <= 43.
+bool gram_fp16_safe(const meq_hparams& hp) {
+  const double a = hp.ns_a, b = hp.ns_b, c = hp.ns_c;
+  double r = 1.0, ma = 1.0, mt = 0.0, mp = 0.0;
+  constexpr int kSamples = 4096;
+  for (int k = 0; k < 64; ++k) {
+    double phimax = 0.0, tmax = 0.0, pmax = 0.0;
+    for (int i = 0; i <= kSamples; ++i) {
+      const double x = r * i / kSamples, l = x * x;
+      const double pl = a + b * l + c * l * l;
+      phimax = std::max(phimax, std::fabs(pl * x));
+      tmax = std::max(tmax, std::fabs(pl * l));
+      pmax = std::max(pmax, std::fabs(pl));
+    }
+    r = 1.02 * phimax;
+    ma = std::max(ma, r * r);
+    mt = std::max(mt, 1.02 * tmax);
+    mp = std::max(mp, 1.02 * pmax);
+    if (!(r < 1e3)) return false;
+  }
+  const double lim = 16384.0;
+  return kGramScale * ma <= lim && kGramScale * mt <= lim && mp * mp * mp <= lim;
+}
+
 // Segments of the K Newton-Schulz steps of one shape group.  A segment of j steps costs, in
 // s^3 units with r = L / S (symmetric products counted once): X X^T r, the j polynomials j,
 // the 3 (j - 1) products P A, P T, P Q, and Q X 2 r; j single steps cost (3 r + 1) j.  With
@@ -79,6 +116,7 @@ struct TimedLaunch {
 struct meq_plan {
   int kind = MEQ_PARAM_HIDDEN;
   meq_hparams hp;
+  bool gram16 = true;  // fp16 Gram and Gram-space matrices (gram_fp16_safe); else the printed bf16 iteration
   std::vector<MatInfo> mats;
   std::vector<GroupInfo> groups;
   size_t off_scal = 0;
@@ -212,6 +250,7 @@ meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hpa
   if (!p) return MEQ_ERR_NO_MEMORY;
   std::unique_ptr<meq_plan> owner(p);  // freed if an allocation below throws
   p->hp = *hp;
+  p->gram16 = gram_fp16_safe(*hp);
   p->mats.resize(count);
   std::map<std::pair<int64_t, int64_t>, int> group_of;
   for (int i = 0; i < count; ++i) {
@@ -265,7 +304,7 @@ meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hpa
     off = align_up(off + 2 * c * g.stride_a, kAlign);
     g.off_p = off;
     off = align_up(off + 2 * c * g.stride_a, kAlign);
-    g.segs = ns_schedule(g.S, g.L, p->hp.ns_steps, p->hp.ns_gram_steps);
+    g.segs = ns_schedule(g.S, g.L, p->hp.ns_steps, p->gram16 ? p->hp.ns_gram_steps : 1);
     const int longest = *std::max_element(g.segs.begin(), g.segs.end());
     g.off_p2 = g.off_t = g.off_q0 = g.off_q1 = 0;
     if (longest >= 2) {
@@ -610,15 +649,6 @@ meq_status enqueue_prescale(meq_plan* p, char* ws, const void* const* grads, flo
 //   OP_APPLY  X' <- P X or Q X                 (NN kernel, K = S)
 enum OpKind { OP_GRAM = 0, OP_POLY = 1, OP_SPROD = 2, OP_APPLY = 3 };
 
-// Gram matrices A = X X^T and the Gram-space matrices are kept in fp16, whose 11-bit
-// significand keeps the S x S iteration more accurate than the printed bf16 step; A and T are
-// stored times kGramScale so that their entries (about 1/s on the diagonal of the first A, and
-// smaller off it) stay in fp16's normal range.  Every entry of A and T is bounded by the largest eigenvalue, at most
-// max (phi^j(sigma))^2 <= 1.45 for A and max sigma phi(sigma) <= 1.21 for T, so the scaled
-// values stay below 1.2e4 (fp16 reaches 65504); P = p(A) and the products Q of P factors are
-// stored unscaled (eigenvalues at most a^3 < 41).
-constexpr float kGramScale = 8192.f;
-
 struct NsOp {
   int kind;
   size_t a, b, c, e;  // workspace offsets: operands, output, added tile (OP_POLY)
@@ -633,26 +663,27 @@ struct NsOp {
 // A = X X^T once; for each step P_i = a I + b A + c A A, then (before the segment's last
 // step) A <- P_i (P_i A), since X P-updated gives (P X)(P X)^T = P A P = P P A; the
 // segment's product Q = P_last ... P_first accumulates alongside; finally X <- Q X.  A
-// one-step segment is exactly A = X X^T, P, X <- P X.  A is always fp16 (scaled by
-// kGramScale); a longer segment also keeps T, its P factors and Q in fp16; the matrix that
+// one-step segment is exactly A = X X^T, P, X <- P X.  With gram16, A is fp16 (scaled by
+// kGramScale) and a longer segment also keeps T, its P factors and Q in fp16; the matrix that
 // feeds the X product (P of a one-step segment, the last Q of a longer one) is bf16, like X.
-// X_0 is in buffer a when x_in_a.
+// Without it (coefficients outside the fp16 range check) every matrix is bf16 and the
+// schedule has only one-step segments.  X_0 is in buffer a when x_in_a.
 std::vector<NsOp> group_ops(const GroupInfo& g, const std::vector<int>& segs, bool x_in_a, bool first_fold,
-                            bool rowcol, const meq_hparams& hp) {
+                            bool rowcol, const meq_hparams& hp, bool gram16) {
   std::vector<NsOp> ops;
   size_t cur = x_in_a ? g.off_xa : g.off_xb, nxt = x_in_a ? g.off_xb : g.off_xa;
   const size_t pbuf[2] = {g.off_p, g.off_p2}, qbuf[2] = {g.off_q0, g.off_q1};
   for (size_t si = 0; si < segs.size(); ++si) {
     const bool fold = first_fold && si == 0;
     const int len = segs[si];
-    const bool f16 = len >= 2;  // P factors in fp16 (they feed fp16 products, not the X product)
-    const float sc = kGramScale;
-    ops.push_back({OP_GRAM, cur, cur, g.off_a, 0, fold ? 2 : 0, false, false, false, true, sc, 0.f, 0.f});
+    const bool f16 = gram16 && len >= 2;  // P factors in fp16 (they feed fp16 products, not the X product)
+    const float sc = gram16 ? kGramScale : 1.f;
+    ops.push_back({OP_GRAM, cur, cur, g.off_a, 0, fold ? 2 : 0, false, false, false, gram16, sc, 0.f, 0.f});
     size_t q = 0;
     for (int j = 0; j < len; ++j) {
       const size_t pj = pbuf[j % 2];
       // P = a I + (b / sc) A' + (c / sc^2) A' A' for the scaled A' = sc A
-      ops.push_back({OP_POLY, g.off_a, g.off_a, pj, g.off_a, 0, false, false, true, f16, hp.ns_c / (sc * sc),
+      ops.push_back({OP_POLY, g.off_a, g.off_a, pj, g.off_a, 0, false, false, gram16, f16, hp.ns_c / (sc * sc),
                      hp.ns_b / sc, hp.ns_a});
       if (j == 0) {
         q = pj;
@@ -819,7 +850,7 @@ meq_status enqueue_chains(meq_plan* p, char* ws, const std::vector<std::vector<N
 // sums of squares of its output (step a4's partials).
 meq_status enqueue_ns(meq_plan* p, char* ws, bool rowcol, hipStream_t st) {
   std::vector<std::vector<NsOp>> chains;
-  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, g.segs, true, true, rowcol, p->hp));
+  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, g.segs, true, true, rowcol, p->hp, p->gram16));
   return enqueue_chains(p, ws, chains, st);
 }
 
@@ -827,7 +858,8 @@ meq_status enqueue_ns(meq_plan* p, char* ws, bool rowcol, hipStream_t st) {
 // one): iteration k reads buffer a when k is even.
 meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, hipStream_t st) {
   std::vector<std::vector<NsOp>> chains;
-  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, {1}, k % 2 == 0, k == 0, false, p->hp));
+  for (const GroupInfo& g : p->groups)
+    chains.push_back(group_ops(g, {1}, k % 2 == 0, k == 0, false, p->hp, p->gram16));
   return enqueue_chains(p, ws, chains, st);
 }
 

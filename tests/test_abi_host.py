@@ -125,6 +125,18 @@ def test_newton_schulz_schedule(shape, steps, gram, segs):
     assert got == segs and sum(got) == steps
 
 
+@pytest.mark.parametrize("coeffs,segs", [
+    ((3.4445, -4.7750, 2.0315), [3, 2]),   # the paper's quintic: singular values stay below 1.21
+    ((1.5, -0.5, 0.0), [3, 2]),            # the cubic Newton-Schulz step: bounded by 1
+    ((2.0, -0.5, 0.0), [1] * 5),           # grows singular values to about 1.57: fp16 unsafe
+    ((3.0, 0.0, 0.0), [1] * 5),            # divergent
+])
+def test_schedule_falls_back_when_fp16_is_unsafe(coeffs, segs):
+    a, b, c = coeffs
+    plan = meq.Plan([(256, 512)], "bf16", hparams=meq.default_hparams(ns_a=a, ns_b=b, ns_c=c))
+    assert plan.schedule(0) == segs
+
+
 def test_schedule_of_the_1b_shapes_and_workspace():
     wl = workloads.workload("llama-1b")
     shapes = [(m.rows, m.cols) for m in wl.matrices]

@@ -63,6 +63,18 @@ def test_newton_schulz_schedules(steps, gram):
     assert all(sum(sg) == steps for sg in segs)
 
 
+@pytest.mark.parametrize("coeffs", [(2.0, -0.5, 0.0), (1.5, -0.5, 0.0)])
+def test_other_ns_coefficients(coeffs):
+    """Coefficients other than the paper's: the cubic step (bounded, fp16 Gram-space segments) and
+    one that grows singular values past the fp16 range check (every matrix through the printed
+    iteration in bf16), against the oracle's iteration with the same coefficients."""
+    a, b, c = coeffs
+    wl = workloads.custom([(256, 768), (1376, 512), (512, 512)], "bf16", name=f"coeffs-{a}-{b}-{c}")
+    hp = meq.default_hparams(ns_a=a, ns_b=b, ns_c=c)
+    run, _ = run_and_check(wl, range(3), steps=2, hp=hp, label=f"coefficients {coeffs}")
+    log(f"[case] schedules {[run.upd.plan.schedule(g) for g in range(len(run.upd.plan.groups()))]}")
+
+
 def test_llama130m_subset_ten_steps():
     wl = workloads.workload("llama-130m")
     # q, k, v, o, gate, up, down of layer 0 and the down projection of the last layer
