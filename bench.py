@@ -182,9 +182,10 @@ XCDS = 8
 def ns_launch_flops(wl) -> dict:
     """Per step, for each NS kernel instantiation over all shape groups: (algorithmic symmetric-aware
     flops, flops the 256 x 256 tiles execute, padding and the lower half of diagonal tiles
-    included), under the default schedule of each shape group: X X^T runs in k_ns_gemm<0, false>,
-    the Gram-space products of multi-step segments in k_ns_gemm<0, true>, the polynomial of a
-    one-step segment in k_ns_gemm<1, false> and of a longer one in k_ns_gemm<1, true>."""
+    included), under the default schedule and coefficients: X X^T runs in k_ns_gemm<0, false>
+    (bf16 X, fp16 output), the Gram-space products in k_ns_gemm<0, true> and every polynomial in
+    k_ns_gemm<1, true> (fp16 A); k_ns_gemm<1, false> only runs for coefficients that fail the fp16
+    range check."""
     from paper_2609_35701_amd import meq
 
     plan = meq.Plan([(m.rows, m.cols) for m in wl.matrices], wl.param_dtype)
@@ -198,8 +199,8 @@ def ns_launch_flops(wl) -> dict:
         sg = segs[(s, l)]
         nseg = len(sg)
         nsprod = sum(3 * (j - 1) for j in sg)
-        poly16 = sum(j for j in sg if j > 1)
-        poly_bf = sum(j for j in sg if j == 1)
+        poly16 = sum(sg)
+        poly_bf = 0
         for k, alg, exe in (("k_ns_gemm<0, false>", nseg * s * s * l, nseg * tri * 2 * 256 * 256 * lp),
                             ("k_ns_gemm<0, true>", nsprod * s ** 3, nsprod * tri * 2 * 256 * 256 * sp),
                             ("k_ns_gemm<1, false>", poly_bf * s ** 3, poly_bf * tri * 2 * 256 * 256 * sp),
@@ -243,6 +244,8 @@ def summarize_mfma(run_dir: str, out: str, command: str, workload: str, note: st
         "|---|---|---|---|---|---|---|---|\n",
     ]
     for k in NS_KERNELS:
+        if k not in tot["GRBM_GUI_ACTIVE"] and flops[k][0] == 0:
+            continue  # not launched under the default coefficients
         gui, n = tot["GRBM_GUI_ACTIVE"].get(k, (float("nan"), 0))
         cyc = gui / XCDS / steps
         busy = tot["SQ_VALU_MFMA_BUSY_CYCLES"].get(k, (float("nan"), 0))[0] / SIMDS / steps / cyc
