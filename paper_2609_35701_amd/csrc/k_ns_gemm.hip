@@ -1,4 +1,4 @@
-// Newton-Schulz products on bf16 MFMA (gfx950), eq. "ns":
+// Newton-Schulz products on MFMA (gfx950), eq. "ns":
 //   A_k = X_k X_k^T                (NT, symmetric: tiles on or above the diagonal + mirrored store)
 //   P_k = a I + b A_k + c A_k A_k  (NT since A_k is symmetric; symmetric output)
 //   X_{k+1} = P_k X_k              (NN: X_k is staged K-major and read with LDS transpose reads)
@@ -8,9 +8,12 @@
 // P_k A_k, P_k T and P_k Q (commuting symmetric factors), and the NN product X <- Q X.
 // X_0 = V / ||V||_F is folded in: the bf16 buffer holds V, the k = 0 Gram epilogue
 // scales by 1/||V||^2 and the k = 0 apply epilogue by 1/||V||.
+// Formats: X and the matrix multiplying it are bf16 (v_mfma_f32_32x32x16_bf16); A and the
+// other S x S matrices may be fp16 (kF16: v_mfma_f32_32x32x16_f16); each product stores its
+// output as bf16 or fp16 (per shape group, GemmGroup::out_f16) with per-group coefficients.
 //
 // One workgroup = 4 waves = one 256 x 256 output tile; each wave owns a 128 x 128
-// quadrant as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation in AGPRs).
+// quadrant as 4 x 4 blocks of 32 x 32 x 16 MFMAs (fp32 accumulation in AGPRs).
 // K advances in slabs of 64 through an LDS ring: operand A in 2 buffers and operand B in 3
 // buffers of 32 KiB, so B is fetched a slab further ahead; that is all of the 160 KiB of
 // LDS.  This measured faster for all three products than a 4-stage ring of 32-wide slabs,
