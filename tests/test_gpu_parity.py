@@ -279,3 +279,49 @@ def test_full_launch_sampled_parity(name):
         assert torch.isfinite(params[i].float()).all()
         assert gr[i] >= 0 and gc[i] >= 0
     assert torch.equal(upd.momenta[5], grads[5].float())
+
+
+@pytest.mark.parametrize("shape", [(16384, 49152), (30000, 10000)])
+def test_largest_shapes_properties(shape):
+    """Shapes far beyond the workloads (the wide one at the 2^31-byte buffer limit's scale, the
+    tall one ragged on both sides), checked through properties that hold at any size, since the
+    fp64 oracle cannot run there: after one step from zero momentum B = G exactly; W stays finite;
+    the balance condition (every nonzero row of U~ has RMS 1 for the row direction, every
+    nonzero column for the column direction) holds for the applied update
+    (W' - (1 - lr lambda) W) / (-rho lr) up to the rounding of W'; U's largest singular value and
+    mean squared singular value lie in the band the quintic maps normalized singular values to."""
+    m, n = shape
+    log(f"[case] largest shapes {shape}")
+    wl = workloads.custom([shape], "bf16", name=f"large-{m}x{n}")
+    params, grads, _ = workloads.device_inputs(wl, DEV)
+    w0 = params[0].clone()
+    upd = meq.HiddenWeightUpdate(params)
+    log(f"[case]   schedule {upd.plan.schedule(0)}, workspace {upd.plan.workspace_bytes / 2**30:.2f} GiB")
+    upd.step(grads, LR)
+    torch.cuda.synchronize()
+    gr, gc, d = upd.stats()
+    assert torch.equal(upd.momenta[0], grads[0].float())
+    w1 = params[0].float()
+    assert torch.isfinite(w1).all()
+    hp = oracle_hp(upd.plan.hparams)
+    decay = float(np.float32(1.0 - np.float64(np.float32(LR)) * np.float64(hp.weight_decay)))
+    step = float(np.float32(np.float64(hp.rho) * np.float64(np.float32(LR))))
+    ut = (w1.double() - decay * w0.double()) / (-step)  # U~ plus the rounding of W'
+    dim = 1 if d[0] == meq.MEQ_DIR_ROW else 0
+    rms = ut.pow(2).mean(dim=dim).sqrt()
+    nz = rms > 0.5
+    log(f"[case]   direction {d[0]}, CVs {gr[0]:.4f} / {gc[0]:.4f}, nonzero lines {int(nz.sum())} of {rms.numel()}, "
+        f"RMS range {float(rms[nz].min()):.5f} .. {float(rms[nz].max()):.5f}")
+    assert int(nz.sum()) == rms.numel()
+    assert float((rms[nz] - 1.0).abs().max()) < 1e-2
+    # singular values of U (wide orientation, bf16 buffer): power iteration in fp32 for the largest
+    u = upd.view(0, meq.BUF_U).float()
+    v = torch.randn(u.shape[1], 1, device=DEV, generator=torch.Generator(device=DEV).manual_seed(3))
+    for _ in range(30):
+        v = u.T @ (u @ v)
+        v = v / v.norm()
+    smax = float((u @ v).norm())
+    msq = float(u.pow(2).sum() / u.shape[0])
+    log(f"[case]   U: largest singular value {smax:.4f}, mean squared singular value {msq:.4f}")
+    assert 0.68 <= smax <= 1.21
+    assert 0.4 <= msq <= 1.45
