@@ -320,3 +320,55 @@ def test_round_bf16_against_torch_and_ties():
     assert oracle.round_bf16(np.array([one + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
     assert oracle.round_bf16(np.array([one + 2 ** -8 + 2 ** -30]))[0] == 1.0 + 2 ** -7
     assert oracle.round_bf16(np.array([-(one + 2 ** -8)]))[0] == -1.0
+
+
+def _gram_space_ns(h, a, b, c, segs):
+    """The Gram-space regrouping of eq. "ns" (reading R21), written out in fp64 for this test
+    only: per segment A = X X^T, then for each step P = a I + b A + c A A, A <- P (P A) and
+    Q <- P Q, and finally X <- Q X."""
+    x = np.asarray(h, np.float64) / np.linalg.norm(h)
+    eye = np.eye(x.shape[0])
+    for seg in segs:
+        am = x @ x.T
+        q = eye
+        for j in range(seg):
+            p = a * eye + b * am + c * (am @ am)
+            q = p @ q
+            if j + 1 < seg:
+                am = p @ (p @ am)
+        x = q @ x
+    return x
+
+
+@pytest.mark.parametrize("segs", [[1] * 5, [2, 2, 1], [3, 2], [2, 3], [5], [4, 1]])
+@pytest.mark.parametrize("shape", [(24, 96), (40, 40), (7, 300)])
+def test_R21_gram_space_regrouping_is_exact(shape, segs):
+    """Every segmentation of the five steps equals the printed iteration up to fp64 rounding:
+    the factors of a segment are polynomials of its first Gram matrix, so they commute and
+    X_{k+1} X_{k+1}^T = P_k A_k P_k.  A wrong update (A <- P A instead of P (P A), or Q
+    accumulated as Q P with a non-commuting factor) breaks it on the wide shapes."""
+    g = rng(31).standard_normal(shape) * np.exp(rng(32).standard_normal((shape[0], 1)))
+    want = oracle.newton_schulz(g, A, B, C, 5)
+    got = _gram_space_ns(g, A, B, C, segs)
+    assert np.linalg.norm(got - want) <= 1e-10 * np.linalg.norm(want)
+
+
+def test_R21_planted_mistakes_fail():
+    g = rng(33).standard_normal((24, 96)) * np.exp(rng(34).standard_normal((24, 1)))
+    want = oracle.newton_schulz(g, A, B, C, 5)
+
+    def wrong_update(h, segs):  # A <- P A: one factor of P missing
+        x = h / np.linalg.norm(h)
+        eye = np.eye(x.shape[0])
+        for seg in segs:
+            am, q = x @ x.T, eye
+            for j in range(seg):
+                p = A * eye + B * am + C * (am @ am)
+                q = p @ q
+                if j + 1 < seg:
+                    am = p @ am
+            x = q @ x
+        return x
+
+    assert np.linalg.norm(wrong_update(g, [3, 2]) - want) > 1e-2 * np.linalg.norm(want)
+    assert np.linalg.norm(_gram_space_ns(g, A, B, C, [3, 2]) - want) <= 1e-10 * np.linalg.norm(want)
