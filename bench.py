@@ -610,6 +610,8 @@ def main() -> int:
         "config": {"workload": wl.name, "matrices": wl.count, "elements": wl.elements,
                    "param_dtype": wl.param_dtype, "grad_dtype": wl.param_dtype, "momentum_dtype": "f32",
                    "ns_steps": hp.ns_steps, "ns_gram_steps": hp.ns_gram_steps,
+                   "ns_operands": "bf16 X and the P or Q multiplying it; fp16 A = X X^T and Gram-space "
+                                  "matrices; fp32 accumulation",
                    "ns_schedules": {f"{k[0]}x{k[1]}": v for k, v in sched.items()},
                    "ns_tflop_per_step": fl["total"] / 1e12,
                    "ns_tflop_per_step_printed_sym": fl["printed"] / 1e12,
