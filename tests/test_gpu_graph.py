@@ -1,0 +1,79 @@
+"""meq_step captured in a HIP graph (torch.cuda.CUDAGraph): the step only enqueues kernels (no
+allocation, memset, copy or synchronization), so a caller may capture it and replay it.  Every
+replay must equal the eager step bitwise (all reductions are fixed-order)."""
+import pytest
+import torch
+
+from paper_2609_35701_amd import meq
+
+pytestmark = pytest.mark.gpu
+
+
+def _seeded(shape, seed, scale, dtype, dev):
+    gen = torch.Generator(device="cpu").manual_seed(seed)
+    return (torch.randn(shape, generator=gen) * scale).to(dtype).to(dev)
+
+
+def test_step_captured_in_a_graph_replays_like_eager():
+    dev = torch.device("cuda:0")
+    # hidden: a Gram-space wide matrix, a tall one, a square one (printed steps), a ragged one;
+    # aux (two-sided) and vector (global RMS) kinds in the same graph
+    hidden_shapes = [(256, 1024), (1024, 256), (512, 512), (300, 100)]
+    aux_shapes = [(700, 64)]
+    vec_shapes = [(1000,), (64,)]
+    kinds = [("hidden", hidden_shapes, meq.HiddenWeightUpdate), ("aux", aux_shapes, meq.AuxUpdate),
+             ("vector", vec_shapes, meq.VectorUpdate)]
+    steps, lr = 3, 0.02
+    grads = {name: [[_seeded(s, 1000 * k + 10 * i + j, 1e-3, torch.bfloat16, dev) for j, s in enumerate(shapes)]
+                    for k in range(steps)] for i, (name, shapes, _) in enumerate(kinds)}
+
+    def build():
+        ups = {}
+        for i, (name, shapes, cls) in enumerate(kinds):
+            params = [_seeded(s, 7 + 10 * i + j, 0.02, torch.bfloat16, dev) for j, s in enumerate(shapes)]
+            ups[name] = cls(params, meq.default_hparams())
+        return ups
+
+    # eager reference
+    eager = build()
+    static_e = {name: [torch.empty_like(g) for g in grads[name][0]] for name, _, _ in kinds}
+    ref = []
+    for k in range(steps):
+        for name, _, _ in kinds:
+            for dst, src in zip(static_e[name], grads[name][k]):
+                dst.copy_(src)
+            eager[name].step(static_e[name], lr)
+        torch.cuda.synchronize()
+        ref.append({name: ([p.clone() for p in u.params], [b.clone() for b in u.momenta])
+                    for name, u in eager.items()})
+
+    # the same three steps as replays of one captured step
+    ups = build()
+    static = {name: [torch.zeros_like(g) for g in grads[name][0]] for name, _, _ in kinds}
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for name, _, _ in kinds:
+            ups[name].step(static[name], lr)
+    torch.cuda.synchronize()
+    # capture ran nothing: parameters and momenta are still the initial ones
+    fresh = build()
+    for name, _, _ in kinds:
+        for p, q in zip(ups[name].params, fresh[name].params):
+            assert torch.equal(p, q)
+        assert all(int(torch.count_nonzero(b)) == 0 for b in ups[name].momenta)
+    del fresh
+    for k in range(steps):
+        for name, _, _ in kinds:  # the program's own eager work between replays
+            for dst, src in zip(static[name], grads[name][k]):
+                dst.copy_(src)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, _, _ in kinds:
+            ps, bs = ref[k][name]
+            for j, (p, q) in enumerate(zip(ups[name].params, ps)):
+                assert torch.equal(p, q), f"replay {k}: {name} parameter {j} differs from the eager step"
+            for j, (b, c) in enumerate(zip(ups[name].momenta, bs)):
+                assert torch.equal(b, c), f"replay {k}: {name} momentum {j} differs from the eager step"
+    graph.reset()
