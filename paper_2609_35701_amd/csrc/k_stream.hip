@@ -57,10 +57,16 @@ __device__ __forceinline__ T block_sum256(T v, T* red /* >= 4 entries */) {
   return r;
 }
 
+// The matrix whose tile range [tile_start[mi], tile_start[mi + 1]) holds block bid (binary
+// search over the launch's prefix sums; tile_start[0] = 0 <= bid).
 __device__ __forceinline__ int find_matrix(const int* tile_start, int count, int bid) {
-  int mi = 0;
-  while (mi + 1 < count && bid >= tile_start[mi + 1]) ++mi;
-  return mi;
+  int lo = 0, hi = count - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (bid >= tile_start[mid]) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
 }
 
 // Eight consecutive floats of a bf16 or fp32 array (16- or 32-byte access).

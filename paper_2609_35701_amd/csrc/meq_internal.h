@@ -14,8 +14,11 @@ constexpr int kTile = 256;
 // orientation; each thread owns 8 consecutive columns of 4 rows.
 constexpr int kEwRows = 64;
 constexpr int kEwCols = 128;
-// Matrices per launch of the multi-matrix element-wise kernels (pointers travel as kernel arguments).
-constexpr int kMaxChunk = 32;
+// Matrices per launch of the multi-matrix element-wise kernels.  Their per-matrix pointers and
+// sizes travel as kernel arguments: at most about 10 KB per launch at this count (ROCm passes
+// argument blocks well beyond the traditional 4 KB; 32 KB was checked on gfx950), so the 1B
+// step's 112 matrices take one launch per stage and no launch ends in a partial wave per chunk.
+constexpr int kMaxChunk = 128;
 
 // Per-matrix scalars kept at the start of the workspace.
 struct MatScalars {
