@@ -1,0 +1,66 @@
+"""Plans side by side on one stream, and the learning-rate edge: the C ABI keeps every plan's
+state in its own workspace and momenta, and lr = 0 leaves the parameters untouched
+(eq. "meqmuon-update" with eta = 0 applies neither the decay nor the step)."""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+
+from gpu_support import Run, log, oracle_hp, to_dev, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def test_zero_learning_rate_leaves_parameters_and_advances_momentum():
+    log("[case] lr = 0")
+    for dtype in ("f32", "bf16"):
+        wl = workloads.custom([(200, 96), (96, 640)], dtype, name=f"lr0-{dtype}", seed=31)
+        run = Run(wl, [0, 1])
+        w0 = [p.clone() for p in run.params]
+        for _ in range(2):
+            grads = run.step(0.0)
+        for k in range(2):
+            assert torch.equal(run.params[k], w0[k]), f"{dtype}: parameter {k} changed with lr = 0"
+        # momentum after two steps: mu G_0 + G_1 in fp32 (one fused multiply-add: within half an
+        # fp32 ulp of the exact value, which float64 holds here up to its own rounding)
+        hp = oracle_hp(run.hp)
+        for k in range(2):
+            g0 = workloads.grad_at_step(wl, k, 0).astype(np.float32)
+            g1 = grads[k].astype(np.float32)
+            if dtype == "bf16":
+                g0 = to_np(to_dev(g0, "bf16"))
+                g1 = to_np(to_dev(g1, "bf16"))
+            want = hp.mu * g0.astype(np.float64) + g1.astype(np.float64)
+            np.testing.assert_allclose(to_np(run.upd.momenta[k]), want, rtol=6.1e-8, atol=0)
+
+
+def test_two_plans_interleaved_on_one_stream_match_sequential_runs():
+    log("[case] two plans interleaved")
+    wl_a = workloads.custom([(256, 1024), (300, 100)], "bf16", name="plan-a", seed=41)
+    wl_b = workloads.custom([(512, 512), (1024, 256), (7, 5)], "bf16", name="plan-b", seed=42)
+
+    def fresh():
+        return Run(wl_a, [0, 1]), Run(wl_b, [0, 1, 2])
+
+    grads = {name: [[to_dev(workloads.grad_at_step(wl, i, s), "bf16") for i in range(wl.count)]
+                    for s in range(3)] for name, wl in (("a", wl_a), ("b", wl_b))}
+    # one plan after the other, synchronized
+    ra, rb = fresh()
+    for s in range(3):
+        ra.upd.step(grads["a"][s], 0.02)
+    torch.cuda.synchronize()
+    for s in range(3):
+        rb.upd.step(grads["b"][s], 0.02)
+    torch.cuda.synchronize()
+    # interleaved step by step on the same stream, no synchronization in between
+    ia, ib = fresh()
+    for s in range(3):
+        ia.upd.step(grads["a"][s], 0.02)
+        ib.upd.step(grads["b"][s], 0.02)
+    torch.cuda.synchronize()
+    for x, y in ((ra, ia), (rb, ib)):
+        for k in range(len(x.params)):
+            assert torch.equal(x.params[k], y.params[k])
+            assert torch.equal(x.upd.momenta[k], y.upd.momenta[k])
+        assert x.upd.stats() == y.upd.stats()
