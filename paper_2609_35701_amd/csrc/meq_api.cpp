@@ -1086,9 +1086,9 @@ MEQ_EXPORT meq_status meq_get_timing(meq_plan* plan, int32_t kind, double* total
 MEQ_EXPORT void meq_destroy(meq_plan* plan) {
   if (!plan) return;
   for (const TimedLaunch& tl : plan->pending) {
-    hipEventDestroy(tl.start);
-    hipEventDestroy(tl.stop);
+    (void)hipEventDestroy(tl.start);
+    (void)hipEventDestroy(tl.stop);
   }
-  for (hipEvent_t e : plan->event_pool) hipEventDestroy(e);
+  for (hipEvent_t e : plan->event_pool) (void)hipEventDestroy(e);
   delete plan;
 }
