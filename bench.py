@@ -403,50 +403,75 @@ def library_gemm_leg() -> dict:
     return out
 
 
-def cpu_baseline_leg(wl, lr: float, budget_s: float):
-    """Time the fp64 oracle on one matrix of each distinct shape and scale to a whole step."""
+def _layer_runs(wl):
+    """Index ranges of the workload's identical transformer layers (7 matrices each, q k v o gate up
+    down), or one range over every matrix when the workload is not a layer stack."""
+    per = 7
+    if wl.count % per == 0 and wl.count > per:
+        shapes = [(m.rows, m.cols) for m in wl.matrices]
+        if all(shapes[i] == shapes[i % per] for i in range(wl.count)):
+            return [range(i, i + per) for i in range(0, wl.count, per)]
+    return [range(wl.count)]
+
+
+def time_oracle_layers(wl, lr: float, budget_s: float, max_layers: int | None = None):
+    """Wall time of the fp64 oracle over whole layers of the workload, one full step of each of their
+    matrices in order (momentum from zero, the printed Newton-Schulz iteration in wide orientation,
+    row/column equilibration, write-back), layer after layer until `budget_s` is spent or
+    `max_layers` are done; inputs are generated outside the timed calls.  Returns (seconds, layers
+    timed, layers in the step)."""
     import numpy as np
 
     import oracle
     import workloads
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([int(i.get("num_threads", 1)) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    except Exception:  # pragma: no cover - threadpoolctl missing
-        threads = len(os.sched_getaffinity(0))
     hp = oracle.HParams()
-    first = {}
-    for i, m in enumerate(wl.matrices):
-        first.setdefault((m.rows, m.cols), []).append(i)
-    per_shape = {}
-    spent = 0.0
-    for shape, idxs in sorted(first.items(), key=lambda kv: kv[0][0] * kv[0][1]):
-        i = idxs[0]
-        w0 = workloads.weight_init(wl, i).astype(np.float64)
-        g = workloads.grad_at_step(wl, i, 0).astype(np.float64)
+    layers = _layer_runs(wl)
+    spent, done = 0.0, 0
+    for lay in layers:
+        if max_layers is not None and done >= max_layers:
+            break
+        inputs = [(workloads.weight_init(wl, i).astype(np.float64), workloads.grad_at_step(wl, i, 0).astype(np.float64))
+                  for i in lay]
         t0 = time.perf_counter()
-        oracle.meq_step(w0, g, np.zeros_like(w0), hp, lr, wide=True)
-        dt = time.perf_counter() - t0
-        per_shape[shape] = (dt, len(idxs))
-        spent += dt
+        for w0, g in inputs:
+            oracle.meq_step(w0, g, np.zeros_like(w0), hp, lr, wide=True)
+        spent += time.perf_counter() - t0
+        done += 1
         if spent > budget_s:
             break
-    if len(per_shape) < len(first):
-        return None
-    sec_per_step = sum(dt * n for dt, n in per_shape.values())
-    sample = ", ".join(f"{r}x{c}: {dt:.2f} s x {n}" for (r, c), (dt, n) in per_shape.items())
+    return spent, done, len(layers)
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        return max([int(i.get("num_threads", 1)) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        return len(os.sched_getaffinity(0))
+
+
+def cpu_baseline_leg(wl, lr: float, budget_s: float, full_step: bool = False):
+    """The fp64 oracle on the host cores: whole layers of the step (every layer of a Llama stack has
+    the same seven shapes, so k of the n layers are k/n of the step's work), or with `full_step`
+    every matrix of the step."""
+    threads = blas_threads()
+    spent, done, total = time_oracle_layers(wl, lr, float("inf") if full_step else budget_s)
+    sec_per_step = spent * total / done
+    what = (f"the full {wl.count}-matrix step timed whole" if done == total else
+            f"{done} of the {total} identical {wl.count // total}-matrix layers timed whole ({spent:.1f} s), "
+            f"scaled by {total}/{done} to the full {wl.count}-matrix step")
     return {"value": 1.0 / sec_per_step, "unit": "steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"fp64 numpy oracle, one matrix of each shape timed once (wide-orientation NS), "
-                      f"scaled by shape counts to the full {wl.count}-matrix step: {sample}; "
-                      f"est. {sec_per_step:.1f} s/step",
+            "sample": f"fp64 numpy oracle (printed Newton-Schulz iteration, wide orientation), {what}: "
+                      f"{sec_per_step:.1f} s/step",
+            "seconds_timed": spent, "layers_timed": done, "layers": total,
             "affinity_cores": len(os.sched_getaffinity(0)), "blas_threads": threads,
             "single_core": single_core_leg(lr)}
 
 
 def single_core_leg(lr: float) -> dict:
-    """The oracle with BLAS limited to one thread: the single 256 x 512 fp32 step whole, and the
-    130M-shape step estimated from one matrix of each shape."""
+    """The oracle with BLAS limited to one thread: the single 256 x 512 fp32 step whole, and two whole
+    layers of the 130M-shape step (12 identical layers) scaled to the step."""
     import numpy as np
 
     import oracle
@@ -466,17 +491,9 @@ def single_core_leg(lr: float) -> dict:
         oracle.meq_step(w0, g, np.zeros_like(w0), hp, lr)
         out["single-256x512_s_per_step"] = time.perf_counter() - t0
         wl = workloads.workload("llama-130m")
-        first = {}
-        for i, m in enumerate(wl.matrices):
-            first.setdefault((m.rows, m.cols), []).append(i)
-        est = 0.0
-        for idxs in first.values():
-            w0 = workloads.weight_init(wl, idxs[0]).astype(np.float64)
-            g = workloads.grad_at_step(wl, idxs[0], 0).astype(np.float64)
-            t0 = time.perf_counter()
-            oracle.meq_step(w0, g, np.zeros_like(w0), hp, lr, wide=True)
-            est += (time.perf_counter() - t0) * len(idxs)
-        out["llama-130m_s_per_step_est"] = est
+        spent, done, total = time_oracle_layers(wl, lr, float("inf"), max_layers=2)
+        out["llama-130m_s_per_step"] = spent * total / done
+        out["llama-130m_sample"] = f"{done} of {total} layers timed whole ({spent:.2f} s)"
     return out
 
 
@@ -490,7 +507,10 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the other parameter kinds and the Moonlight-Muon comparison")
-    ap.add_argument("--cpu-budget", type=float, default=30.0, help="seconds of oracle work at most")
+    ap.add_argument("--cpu-budget", type=float, default=30.0,
+                    help="seconds of oracle work at most: whole layers of the step are timed until it is spent")
+    ap.add_argument("--cpu-full-step", action="store_true",
+                    help="time the oracle on every matrix of the step (about 90 s for the 1B shapes)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain copy kernel of known size (torch.neg over 256 MiB of fp32) before the "
                          "warm-up, as the reference for FETCH_SIZE / WRITE_SIZE counter runs")
@@ -535,20 +555,61 @@ def main() -> int:
         return 1
     dev = torch.device("cuda:0")
     wl = workloads.workload(args.workload)
-    print(f"# bench: workload {wl.name}, {wl.count} matrices, {wl.elements} elements", file=sys.stderr, flush=True)
     params, grads, _ = workloads.device_inputs(wl, dev)
+    calib = None
+    if args.copy_calibration:
+        def calib():
+            src = torch.ones(CALIBRATION_BYTES // 4, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            torch.neg(src, out=dst)
+            torch.cuda.synchronize()
+            del src, dst
+    res = measure_workload(wl, params, grads, args.steps, args.warmup, args.lr, before_warmup=calib)
+    extras = None
+    if not args.no_extras and wl.name == "llama-1b":
+        print("# bench: other parameter kinds and the Moonlight-Muon rule", file=sys.stderr, flush=True)
+        extras = extras_leg(params, wl, args.lr, min(args.steps, 20), max(args.warmup, 1))
+        extras["equilibration_overhead_ms"] = res["ms_per_step"] - extras["moonlight_hidden"]["ms_per_step"]
+        extras["library_gemm"] = library_gemm_leg()
+        del params, grads
+        torch.cuda.empty_cache()
+        extras["configs"] = configs_leg(res, args.lr, min(args.steps, 20), args.warmup)
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("# bench: timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
+        cpu = cpu_baseline_leg(wl, args.lr, args.cpu_budget, args.cpu_full_step)
+    line = {
+        "metric": METRIC, "value": 1e3 / res["ms_per_step"], "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": res["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": res["config"],
+        "roofline": res["roofline"], "cpu_baseline": cpu, "stages": res["stages"],
+        "kernels_ms_per_step": res["kernels_ms_per_step"],
+        "kernels_pass": f"{breakdown_steps(args.steps)} steps after the timed region with HIP events around every kernel",
+        "extras": extras,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def measure_workload(wl, params, grads, steps: int, warmup: int, lr: float, before_warmup=None,
+                     tag: str = "bench") -> dict:
+    """One workload's hidden-weight step on the GPU: wall time per step over `steps` timed steps (HIP
+    events around the dominant X products only), then a breakdown pass with events around every
+    kernel, and the flop and byte rates of the step's stages."""
+    import torch
+
+    from paper_2609_35701_amd import meq
+
+    print(f"# {tag}: workload {wl.name}, {wl.count} matrices, {wl.elements} elements", file=sys.stderr, flush=True)
     upd = meq.HiddenWeightUpdate(params)
     hp = upd.plan.hparams
-    print(f"# bench: workspace {upd.plan.workspace_bytes / 2**30:.2f} GiB, groups {upd.plan.groups()}",
+    print(f"# {tag}: workspace {upd.plan.workspace_bytes / 2**30:.2f} GiB, groups {upd.plan.groups()}",
           file=sys.stderr, flush=True)
-    if args.copy_calibration:
-        src = torch.ones(CALIBRATION_BYTES // 4, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.neg(src, out=dst)
-        torch.cuda.synchronize()
-        del src, dst
-    for _ in range(args.warmup):
-        upd.step(grads, args.lr)
+    if before_warmup is not None:
+        before_warmup()
+    for _ in range(warmup):
+        upd.step(grads, lr)
     torch.cuda.synchronize()
     # timed region: HIP events on the launch stream around the dominant kernel (the X product)
     # only; events around every kernel cost about 1% of the step, so the per-kernel breakdown
@@ -558,20 +619,20 @@ def main() -> int:
     upd.plan.get_timing(apply_kind, reset=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        upd.step(grads, args.lr)
+    for _ in range(steps):
+        upd.step(grads, lr)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     upd.plan.set_timing([])
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ms_per_step = (t1 - t0) * 1e3 / steps
     ap_total_ms, ap_n = upd.plan.get_timing(apply_kind)
-    nb = breakdown_steps(args.steps)
+    nb = breakdown_steps(steps)
     upd.plan.set_timing(range(len(meq.KERNEL_NAMES)))
     for k in range(len(meq.KERNEL_NAMES)):
         upd.plan.get_timing(k, reset=True)
     torch.cuda.synchronize()
     for _ in range(nb):
-        upd.step(grads, args.lr)
+        upd.step(grads, lr)
     torch.cuda.synchronize()
     upd.plan.set_timing([])
     kern = {}
@@ -579,8 +640,9 @@ def main() -> int:
         ms, n = upd.plan.get_timing(k)
         kern[name] = {"ms_per_step": ms / nb, "launches_per_step": n / nb,
                       "avg_launch_ms": ms / n if n else None}
-    print(f"# bench: {ms_per_step:.3f} ms/step; breakdown over {nb} more steps: " +
-          ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in kern.items() if v["launches_per_step"]), file=sys.stderr, flush=True)
+    print(f"# {tag}: {ms_per_step:.3f} ms/step; breakdown over {nb} more steps: " +
+          ", ".join(f"{k} {v['ms_per_step']:.3f}" for k, v in kern.items() if v["launches_per_step"]),
+          file=sys.stderr, flush=True)
 
     sched = {(gs, gl): upd.plan.schedule(g) for g, (gs, gl, _) in enumerate(upd.plan.groups())}
     fl = {}
@@ -595,8 +657,8 @@ def main() -> int:
     ns_kinds = ("gram", "poly", "apply")
     ns_ms = sum(kern[k]["ms_per_step"] for k in ns_kinds)
     # the dominant kernel's figures come from the timed region's own events
-    ap_ms = ap_total_ms / args.steps
-    ap_per_step = ap_n / args.steps
+    ap_ms = ap_total_ms / steps
+    ap_per_step = ap_n / steps
     apply_tflops = fl["apply"] / (ap_ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "kernel": f"{APPLY_KERNEL} (X <- P X, or Q X after a Gram-space segment; bf16 MFMA)",
                 "achieved": apply_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -617,36 +679,54 @@ def main() -> int:
     }
     if "rowcol" in sb:
         stages["rowcol_gbs"] = sb["rowcol"] / (kern["rowcol"]["ms_per_step"] * 1e-3) / 1e9
-    extras = None
-    if not args.no_extras and wl.name == "llama-1b":
-        print("# bench: other parameter kinds and the Moonlight-Muon rule", file=sys.stderr, flush=True)
-        extras = extras_leg(params, wl, args.lr, min(args.steps, 20), max(args.warmup, 1))
-        extras["equilibration_overhead_ms"] = ms_per_step - extras["moonlight_hidden"]["ms_per_step"]
-        extras["library_gemm"] = library_gemm_leg()
-    cpu = None
-    if not args.no_cpu_baseline:
-        print("# bench: timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
-        cpu = cpu_baseline_leg(wl, args.lr, args.cpu_budget)
-    line = {
-        "metric": METRIC, "value": 1e3 / ms_per_step, "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": wl.name, "matrices": wl.count, "elements": wl.elements,
-                   "param_dtype": wl.param_dtype, "grad_dtype": wl.param_dtype, "momentum_dtype": "f32",
-                   "ns_steps": hp.ns_steps, "ns_gram_steps": hp.ns_gram_steps,
-                   "ns_operands": "bf16 X and the P or Q multiplying it; fp16 A = X X^T and Gram-space "
-                                  "matrices; fp32 accumulation",
-                   "ns_schedules": {f"{k[0]}x{k[1]}": v for k, v in sched.items()},
-                   "ns_tflop_per_step": fl["total"] / 1e12,
-                   "ns_tflop_per_step_printed_sym": fl["printed"] / 1e12,
-                   "ns_tflop_per_step_printed_dense": fl["dense"] / 1e12},
-        "roofline": roofline, "cpu_baseline": cpu, "stages": stages,
-        "kernels_ms_per_step": {k: v["ms_per_step"] for k, v in kern.items() if v["launches_per_step"]},
-        "kernels_pass": f"{nb} steps after the timed region with HIP events around every kernel",
-        "extras": extras,
-    }
-    print(json.dumps(line), flush=True)
-    return 0
+    config = {"workload": wl.name, "matrices": wl.count, "elements": wl.elements,
+              "param_dtype": wl.param_dtype, "grad_dtype": wl.param_dtype, "momentum_dtype": "f32",
+              "ns_steps": hp.ns_steps, "ns_gram_steps": hp.ns_gram_steps,
+              "ns_operands": "bf16 X and the P or Q multiplying it; fp16 A = X X^T and Gram-space "
+                             "matrices; fp32 accumulation",
+              "ns_schedules": {f"{k[0]}x{k[1]}": v for k, v in sched.items()},
+              "ns_tflop_per_step": fl["total"] / 1e12,
+              "ns_tflop_per_step_printed_sym": fl["printed"] / 1e12,
+              "ns_tflop_per_step_printed_dense": fl["dense"] / 1e12}
+    del upd
+    return {"ms_per_step": ms_per_step, "steps_per_s": 1e3 / ms_per_step, "config": config, "roofline": roofline,
+            "stages": stages, "kernels_ms_per_step": {k: v["ms_per_step"] for k, v in kern.items()
+                                                      if v["launches_per_step"]}}
+
+
+# The workloads of the benchmark's table besides the headline: the single 256 x 512 fp32 matrix,
+# the 130M and 350M Llama shapes and the 7B block x4 with extreme imbalance.
+OTHER_CONFIGS = ("single-256x512", "llama-130m", "llama-350m", "llama-7b-block-x4")
+
+
+def configs_leg(headline: dict, lr: float, steps: int, warmup: int) -> dict:
+    """Every workload of the table on the same build and box: steps/s, the executed-flop NS rate and
+    fraction of the bf16 peak, the X product's fraction, and the byte stages' GB/s."""
+    import torch
+
+    import workloads
+
+    def row(r):
+        st = r["stages"]
+        return {"steps_per_s": r["steps_per_s"], "ms_per_step": r["ms_per_step"],
+                "ns_tflop_per_step": r["config"]["ns_tflop_per_step"],
+                "ns_tflops": st["ns_tflops"], "ns_frac_of_peak": st["ns_frac_of_peak"],
+                "ns_tflops_by_kernel": st["ns_tflops_by_kernel"],
+                "apply_frac": r["roofline"]["frac"],
+                "momentum_gbs": st["momentum_gbs"], "update_gbs": st["update_gbs"],
+                "byte_stages_gbs": st["byte_stages_gbs"],
+                "byte_stages_frac_of_peak": st["byte_stages_gbs"] / PEAK_HBM_GBS,
+                "kernels_ms_per_step": r["kernels_ms_per_step"]}
+
+    out = {"llama-1b": row(headline)}
+    dev = torch.device("cuda:0")
+    for name in OTHER_CONFIGS:
+        wl = workloads.workload(name)
+        params, grads, _ = workloads.device_inputs(wl, dev)
+        out[name] = row(measure_workload(wl, params, grads, steps, warmup, lr, tag=f"config {name}"))
+        del params, grads
+        torch.cuda.empty_cache()
+    return out
 
 
 if __name__ == "__main__":

@@ -161,6 +161,23 @@ meq_status meq_init_kind(int32_t kind, const meq_matrix_desc* mats, int32_t coun
 /* meq_init_kind(MEQ_PARAM_HIDDEN, ...). */
 meq_status meq_init(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out);
 
+/*
+ * meq_init_kind with the plan's workspace held to at most max_workspace_bytes (0: no cap, the
+ * same plan as meq_init_kind).  The update is the same: every matrix's arithmetic is the same,
+ * and the results are bitwise equal to the uncapped plan's.  A hidden plan keeps its per-matrix
+ * statistics for all matrices and one region for the Newton-Schulz buffers
+ * (Algorithm "MeqMuon" as written handles one matrix at a time; the memory of the update is the
+ * point of the paper's Table "experiment-efficiency"): its shape groups are cut into slices
+ * packed into passes that fit the region, and meq_step runs the passes one after the other on
+ * the stream (momentum, Newton-Schulz, statistics and write-back of one pass before the next),
+ * each reusing the region.  Fewer matrices per launch fill the GPU less, so a small cap costs
+ * time.  Aux and vector plans are not sliced; their workspace must fit the cap as planned.
+ * MEQ_ERR_WORKSPACE when the per-matrix part alone, or one matrix's Newton-Schulz buffers,
+ * exceed the cap; other errors as meq_init_kind.
+ */
+meq_status meq_init_capped(int32_t kind, const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp,
+                           size_t max_workspace_bytes, meq_plan** out);
+
 /* Bytes of device workspace meq_step needs for this plan (0 for a null plan). */
 size_t meq_workspace_bytes(const meq_plan* plan);
 
@@ -219,9 +236,14 @@ const char* meq_status_string(meq_status s);
  * Introspection (host only, no device work)
  * ------------------------------------------------------------------------- */
 
-/* Number of Newton-Schulz shape groups (matrices with equal (min, max) dims);
- * 0 for aux and vector plans. */
+/* Number of Newton-Schulz shape groups (matrices with equal (min, max) dims); in a plan from
+ * meq_init_capped a shape group cut into slices counts once per slice.  0 for aux and vector
+ * plans. */
 int32_t meq_plan_num_groups(const meq_plan* plan);
+
+/* Number of passes a hidden plan's step runs (1 without a workspace cap; 0 for an empty plan and
+ * for aux and vector plans). */
+int32_t meq_plan_num_passes(const meq_plan* plan);
 
 /* Shape group g: short side s, long side l (after transposing tall matrices to
  * wide orientation) and its number of matrices. */
@@ -242,8 +264,9 @@ typedef enum {
   MEQ_BUF_X0 = 0,      /* bf16 V (not yet divided by ||V||_F), wide orientation s x l, ld = padded l;
                           still intact after a step only when the matrix's Newton-Schulz schedule
                           has one segment (meq_plan_group_schedule; later segments reuse the
-                          buffer)                                                                */
-  MEQ_BUF_U = 1,       /* bf16 Newton-Schulz output U, wide orientation s x l, ld = padded l          */
+                          buffer) and the matrix is in the plan's last pass                       */
+  MEQ_BUF_U = 1,       /* bf16 Newton-Schulz output U, wide orientation s x l, ld = padded l; after a
+                          step of a plan with several passes only for matrices of the last pass    */
   MEQ_BUF_NORMSQ = 2,  /* double ||V||_F^2, 1 x 1                                                    */
   MEQ_BUF_ROW_RMS = 3, /* double r of U in the matrix's own orientation, 1 x rows                      */
   MEQ_BUF_COL_RMS = 4, /* double c of U in the matrix's own orientation, 1 x cols                      */

@@ -34,7 +34,8 @@ struct MatInfo {
   int64_t m, n, s, l, S, L;
   bool tall;
   int dtype;  // param dtype == grad dtype
-  int group, gidx;
+  int group, gidx;  // group slice (index into meq_plan::groups) and position in it
+  int pass;         // hidden plans: the pass that updates this matrix
   int tiles_pad_r, tiles_pad_c;  // kEwRows x kEwCols tiles over the padded matrix in its own orientation
   int tiles_upd_r, tiles_upd_c;  // kEwRows x kEwCols tiles over the real matrix
   size_t off_part, off_rrms, off_crms, off_scale;
@@ -44,6 +45,7 @@ struct MatInfo {
   size_t off_rscale, off_cscale, off_cpart, off_normsq;
 };
 
+// A shape group, or the slice of one that a pass of a workspace-capped plan updates.
 struct GroupInfo {
   int64_t s, l, S, L;
   std::vector<int> mats;
@@ -106,6 +108,14 @@ std::vector<int> ns_schedule(int64_t S, int64_t L, int steps, int gram_steps) {
 // (each segment ends with one X product that writes the other buffer).
 bool u_in_b(const GroupInfo& g) { return g.segs.size() % 2 == 1; }
 
+// One pass of a hidden plan: group slices whose Newton-Schulz buffers share the workspace's
+// Newton-Schulz region, and their matrices.  An uncapped plan has one pass holding every shape
+// group whole; a capped plan runs its passes one after the other, each reusing the region.
+struct Pass {
+  std::vector<int> groups;
+  std::vector<int> mats;
+};
+
 struct TimedLaunch {
   int kind;
   hipEvent_t start, stop;
@@ -119,6 +129,7 @@ struct meq_plan {
   bool gram16 = true;  // fp16 Gram and Gram-space matrices (gram_fp16_safe); else the printed bf16 iteration
   std::vector<MatInfo> mats;
   std::vector<GroupInfo> groups;
+  std::vector<Pass> passes;
   size_t off_scal = 0;
   size_t ws_bytes = 0;
   uint32_t timing_mask = 0;
@@ -237,8 +248,40 @@ MEQ_EXPORT const char* meq_status_string(meq_status s) {
 
 namespace {
 
-// Hidden 2D weights: shape groups for the Newton-Schulz launches and the workspace layout.
-meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out) {
+// Bytes of one group slice's Newton-Schulz buffers for c matrices, each region 256-byte aligned:
+// the 1/||V|| fold table, two ping-pong X buffers, A and P, the Gram-space buffers its schedule
+// needs, and the row/column sum-of-squares partials.  With `g` the offsets are assigned from `base`.
+size_t slice_layout(GroupInfo* g, int64_t S, int64_t L, size_t c, int longest, size_t base) {
+  const size_t sx = static_cast<size_t>(S * L), sa = static_cast<size_t>(S * S);
+  const size_t srp = static_cast<size_t>((L / kTile) * S), scp = static_cast<size_t>((S / kTile) * L);
+  size_t off = base;
+  auto take = [&](size_t* dst, size_t bytes) {
+    if (dst) *dst = off;
+    off = align_up(off + bytes, kAlign);
+  };
+  take(g ? &g->off_fold : nullptr, 8 * c);
+  take(g ? &g->off_xa : nullptr, 2 * c * sx);
+  take(g ? &g->off_xb : nullptr, 2 * c * sx);
+  take(g ? &g->off_a : nullptr, 2 * c * sa);
+  take(g ? &g->off_p : nullptr, 2 * c * sa);
+  if (g) g->off_p2 = g->off_t = g->off_q0 = g->off_q1 = 0;
+  if (longest >= 2) {
+    take(g ? &g->off_p2 : nullptr, 2 * c * sa);
+    take(g ? &g->off_t : nullptr, 2 * c * sa);
+    take(g ? &g->off_q0 : nullptr, 2 * c * sa);
+  }
+  if (longest >= 3) take(g ? &g->off_q1 : nullptr, 2 * c * sa);
+  take(g ? &g->off_rpart : nullptr, 4 * c * srp);
+  take(g ? &g->off_cpart : nullptr, 4 * c * scp);
+  return off - base;
+}
+
+// Hidden 2D weights: shape groups for the Newton-Schulz launches and the workspace layout.  The
+// workspace holds the per-matrix scalars and vectors, then one Newton-Schulz region.  Without a
+// cap (max_ws == 0) one pass covers every shape group; with one, the groups are cut into slices
+// packed greedily into passes whose region fits the cap.
+meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, size_t max_ws,
+                       meq_plan** out) {
   for (int i = 0; i < count; ++i) {
     const meq_matrix_desc& d = mats[i];
     if (d.rows < 1 || d.cols < 1 || d.rows > kMaxDim || d.cols > kMaxDim) return MEQ_ERR_INVALID_ARG;
@@ -252,7 +295,9 @@ meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hpa
   p->hp = *hp;
   p->gram16 = gram_fp16_safe(*hp);
   p->mats.resize(count);
+  // shape groups in order of first appearance
   std::map<std::pair<int64_t, int64_t>, int> group_of;
+  std::vector<GroupInfo> shapes;
   for (int i = 0; i < count; ++i) {
     MatInfo& mi = p->mats[i];
     mi.m = mats[i].rows;
@@ -271,57 +316,21 @@ meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hpa
     auto key = std::make_pair(mi.s, mi.l);
     auto it = group_of.find(key);
     if (it == group_of.end()) {
-      it = group_of.emplace(key, static_cast<int>(p->groups.size())).first;
+      it = group_of.emplace(key, static_cast<int>(shapes.size())).first;
       GroupInfo g{};
       g.s = mi.s;
       g.l = mi.l;
       g.S = mi.S;
       g.L = mi.L;
-      p->groups.push_back(g);
+      g.segs = ns_schedule(g.S, g.L, p->hp.ns_steps, p->gram16 ? p->hp.ns_gram_steps : 1);
+      shapes.push_back(g);
     }
-    mi.group = it->second;
-    mi.gidx = static_cast<int>(p->groups[mi.group].mats.size());
-    p->groups[mi.group].mats.push_back(i);
+    shapes[it->second].mats.push_back(i);
   }
-  // Workspace layout: per-matrix scalars, then each group's NS buffers, then
-  // per-matrix partials and vectors.  Every region starts 256-byte aligned.
+  // persistent part: per-matrix scalars, tile partials of ||V||^2, r, c and the scale vector
   size_t off = 0;
   p->off_scal = off;
   off = align_up(off + sizeof(MatScalars) * static_cast<size_t>(count), kAlign);
-  for (GroupInfo& g : p->groups) {
-    const size_t c = g.mats.size();
-    g.stride_x = g.S * g.L;
-    g.stride_a = g.S * g.S;
-    g.stride_rpart = (g.L / kTile) * g.S;
-    g.stride_cpart = (g.S / kTile) * g.L;
-    g.off_fold = off;
-    off = align_up(off + 8 * c, kAlign);
-    g.off_xa = off;
-    off = align_up(off + 2 * c * g.stride_x, kAlign);
-    g.off_xb = off;
-    off = align_up(off + 2 * c * g.stride_x, kAlign);
-    g.off_a = off;
-    off = align_up(off + 2 * c * g.stride_a, kAlign);
-    g.off_p = off;
-    off = align_up(off + 2 * c * g.stride_a, kAlign);
-    g.segs = ns_schedule(g.S, g.L, p->hp.ns_steps, p->gram16 ? p->hp.ns_gram_steps : 1);
-    const int longest = *std::max_element(g.segs.begin(), g.segs.end());
-    g.off_p2 = g.off_t = g.off_q0 = g.off_q1 = 0;
-    if (longest >= 2) {
-      for (size_t* o : {&g.off_p2, &g.off_t, &g.off_q0}) {
-        *o = off;
-        off = align_up(off + 2 * c * g.stride_a, kAlign);
-      }
-    }
-    if (longest >= 3) {
-      g.off_q1 = off;
-      off = align_up(off + 2 * c * g.stride_a, kAlign);
-    }
-    g.off_rpart = off;
-    off = align_up(off + 4 * c * g.stride_rpart, kAlign);
-    g.off_cpart = off;
-    off = align_up(off + 4 * c * g.stride_cpart, kAlign);
-  }
   for (MatInfo& mi : p->mats) {
     mi.off_part = off;
     off = align_up(off + 4 * static_cast<size_t>(mi.tiles_pad_r) * mi.tiles_pad_c, kAlign);
@@ -332,7 +341,52 @@ meq_status init_hidden(const meq_matrix_desc* mats, int32_t count, const meq_hpa
     mi.off_scale = off;
     off = align_up(off + 4 * static_cast<size_t>(std::max(mi.m, mi.n)), kAlign);
   }
-  p->ws_bytes = off;
+  const size_t off_ns = off;
+  if (max_ws != 0 && off_ns > max_ws) return MEQ_ERR_WORKSPACE;
+  const size_t room = max_ws == 0 ? SIZE_MAX : max_ws - off_ns;
+  // group slices packed into passes
+  size_t used = 0, region = 0;
+  p->passes.emplace_back();
+  for (const GroupInfo& sg : shapes) {
+    const int longest = *std::max_element(sg.segs.begin(), sg.segs.end());
+    size_t next = 0;
+    while (next < sg.mats.size()) {
+      const size_t left = sg.mats.size() - next;
+      size_t c = left;
+      while (c > 0 && used + slice_layout(nullptr, sg.S, sg.L, c, longest, 0) > room) c = c * 2 / 3;
+      while (c < left && used + slice_layout(nullptr, sg.S, sg.L, c + 1, longest, 0) <= room) ++c;
+      if (c == 0) {
+        if (used == 0) return MEQ_ERR_WORKSPACE;  // not even one matrix of this shape fits
+        p->passes.emplace_back();
+        used = 0;
+        continue;
+      }
+      GroupInfo g = sg;
+      g.mats.assign(sg.mats.begin() + static_cast<std::ptrdiff_t>(next),
+                    sg.mats.begin() + static_cast<std::ptrdiff_t>(next + c));
+      g.stride_x = g.S * g.L;
+      g.stride_a = g.S * g.S;
+      g.stride_rpart = (g.L / kTile) * g.S;
+      g.stride_cpart = (g.S / kTile) * g.L;
+      used += slice_layout(&g, g.S, g.L, c, longest, off_ns + used);
+      region = std::max(region, used);
+      const int gi = static_cast<int>(p->groups.size());
+      for (size_t k = 0; k < g.mats.size(); ++k) {
+        MatInfo& mi = p->mats[g.mats[k]];
+        mi.group = gi;
+        mi.gidx = static_cast<int>(k);
+        mi.pass = static_cast<int>(p->passes.size()) - 1;
+        p->passes.back().mats.push_back(g.mats[k]);
+      }
+      p->passes.back().groups.push_back(gi);
+      p->groups.push_back(std::move(g));
+      next += c;
+    }
+  }
+  if (p->passes.back().groups.empty()) p->passes.pop_back();
+  // matrices of a pass in their plan order (the launch chunks follow it)
+  for (Pass& ps : p->passes) std::sort(ps.mats.begin(), ps.mats.end());
+  p->ws_bytes = off_ns + region;
   *out = owner.release();
   return MEQ_OK;
 }
@@ -386,16 +440,37 @@ meq_status init_stream_kind(int32_t kind, const meq_matrix_desc* mats, int32_t c
 
 }  // namespace
 
-MEQ_EXPORT meq_status meq_init_kind(int32_t kind, const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp,
-                                    meq_plan** out) {
+namespace {
+
+meq_status init_any(int32_t kind, const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, size_t max_ws,
+                    meq_plan** out) {
   if (out) *out = nullptr;
   if (!out || !hp || count < 0 || (count > 0 && !mats)) return MEQ_ERR_INVALID_ARG;
   if (kind != MEQ_PARAM_HIDDEN && kind != MEQ_PARAM_AUX && kind != MEQ_PARAM_VECTOR) return MEQ_ERR_INVALID_ARG;
   MEQ_TRY(validate_hparams(*hp));
   if (hp->update_rule != MEQ_RULE_MEQMUON && kind != MEQ_PARAM_HIDDEN) return MEQ_ERR_INVALID_ARG;
-  return guarded([&] {
-    return kind == MEQ_PARAM_HIDDEN ? init_hidden(mats, count, hp, out) : init_stream_kind(kind, mats, count, hp, out);
+  return guarded([&]() -> meq_status {
+    if (kind == MEQ_PARAM_HIDDEN) return init_hidden(mats, count, hp, max_ws, out);
+    MEQ_TRY(init_stream_kind(kind, mats, count, hp, out));
+    if (max_ws != 0 && (*out)->ws_bytes > max_ws) {
+      delete *out;
+      *out = nullptr;
+      return MEQ_ERR_WORKSPACE;
+    }
+    return MEQ_OK;
   });
+}
+
+}  // namespace
+
+MEQ_EXPORT meq_status meq_init_kind(int32_t kind, const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp,
+                                    meq_plan** out) {
+  return init_any(kind, mats, count, hp, 0, out);
+}
+
+MEQ_EXPORT meq_status meq_init_capped(int32_t kind, const meq_matrix_desc* mats, int32_t count,
+                                      const meq_hparams* hp, size_t max_workspace_bytes, meq_plan** out) {
+  return init_any(kind, mats, count, hp, max_workspace_bytes, out);
 }
 
 MEQ_EXPORT meq_status meq_init(const meq_matrix_desc* mats, int32_t count, const meq_hparams* hp, meq_plan** out) {
@@ -406,6 +481,10 @@ MEQ_EXPORT size_t meq_workspace_bytes(const meq_plan* plan) { return plan ? plan
 
 MEQ_EXPORT int32_t meq_plan_num_groups(const meq_plan* plan) {
   return plan ? static_cast<int32_t>(plan->groups.size()) : 0;
+}
+
+MEQ_EXPORT int32_t meq_plan_num_passes(const meq_plan* plan) {
+  return plan && plan->kind == MEQ_PARAM_HIDDEN ? static_cast<int32_t>(plan->passes.size()) : 0;
 }
 
 MEQ_EXPORT meq_status meq_plan_group(const meq_plan* plan, int32_t g, int64_t* s, int64_t* l, int32_t* count) {
@@ -573,12 +652,11 @@ meq_status step_vec(meq_plan* p, void* const* params, const void* const* grads, 
 namespace {
 
 // Element-wise kernels run over chunks of matrices sharing a dtype.
-std::vector<std::vector<int>> dtype_chunks(const meq_plan* p) {
-  const int count = static_cast<int>(p->mats.size());
+std::vector<std::vector<int>> dtype_chunks(const meq_plan* p, const std::vector<int>& mats) {
   std::vector<std::vector<int>> chunks;
   for (int dt = 0; dt < 2; ++dt) {
     std::vector<int> cur;
-    for (int i = 0; i < count; ++i) {
+    for (int i : mats) {
       if (p->mats[i].dtype != dt) continue;
       cur.push_back(i);
       if (static_cast<int>(cur.size()) == kMaxChunk) {
@@ -591,13 +669,22 @@ std::vector<std::vector<int>> dtype_chunks(const meq_plan* p) {
   return chunks;
 }
 
+// Matrices of a pass in chunks of at most kMaxChunk (any dtype).
+std::vector<std::vector<int>> plain_chunks(const std::vector<int>& mats) {
+  std::vector<std::vector<int>> chunks;
+  for (size_t c0 = 0; c0 < mats.size(); c0 += kMaxChunk)
+    chunks.emplace_back(mats.begin() + static_cast<std::ptrdiff_t>(c0),
+                        mats.begin() + static_cast<std::ptrdiff_t>(std::min(mats.size(), c0 + kMaxChunk)));
+  return chunks;
+}
+
 // Steps a1-a2: momentum (or, with momenta == nullptr, V = the given inputs), bf16 V in wide
 // orientation, ||V||_F^2 and its reciprocals.
-meq_status enqueue_prescale(meq_plan* p, char* ws, const void* const* grads, float* const* momenta, hipStream_t st) {
+meq_status enqueue_prescale(meq_plan* p, const Pass& ps, char* ws, const void* const* grads, float* const* momenta,
+                            hipStream_t st) {
   const meq_hparams& hp = p->hp;
-  const int count = static_cast<int>(p->mats.size());
   MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
-  const auto chunks = dtype_chunks(p);
+  const auto chunks = dtype_chunks(p, ps.mats);
   // 1. momentum + bf16 V (wide, zero-padded) + per-tile ||V||^2 partials
   for (const auto& ch : chunks) {
     MomentumArgs a{};
@@ -626,14 +713,14 @@ meq_status enqueue_prescale(meq_plan* p, char* ws, const void* const* grads, flo
     MEQ_TRY(timed_launch(p, MEQ_K_MOMENTUM, st, [&] { return launch_momentum(a, gbf, tiles, st); }));
   }
   // 2. ||V||_F^2 and its reciprocals
-  for (int c0 = 0; c0 < count; c0 += kMaxChunk) {
+  for (const auto& ch : plain_chunks(ps.mats)) {
     NormArgs a{};
-    a.count = std::min(kMaxChunk, count - c0);
+    a.count = static_cast<int>(ch.size());
     for (int k = 0; k < a.count; ++k) {
-      const MatInfo& mi = p->mats[c0 + k];
+      const MatInfo& mi = p->mats[ch[k]];
       a.nparts[k] = mi.tiles_pad_r * mi.tiles_pad_c;
       a.part[k] = reinterpret_cast<const float*>(ws + mi.off_part);
-      a.scal[k] = scal + c0 + k;
+      a.scal[k] = scal + ch[k];
       a.fold[k] = reinterpret_cast<float*>(ws + p->groups[mi.group].off_fold) + 2 * mi.gidx;
     }
     MEQ_TRY(timed_launch(p, MEQ_K_NORM, st, [&] { return launch_norm(a, st); }));
@@ -803,11 +890,12 @@ std::vector<Bundle> merge_launches(const std::vector<Bundle>& a, const std::vect
 // Enqueue the chains of all groups: the heaviest chain first, the others merged into its launch
 // sequence; each launch runs its entries in grouped launches of up to kMaxGemmGroups, longest K
 // first so the long tiles start first.
-meq_status enqueue_chains(meq_plan* p, char* ws, const std::vector<std::vector<NsOp>>& chains, hipStream_t st) {
-  auto chain_work = [&](size_t gi) {
-    const GroupInfo& g = p->groups[gi];
+meq_status enqueue_chains(meq_plan* p, char* ws, const std::vector<int>& gids,
+                          const std::vector<std::vector<NsOp>>& chains, hipStream_t st) {
+  auto chain_work = [&](size_t c) {
+    const GroupInfo& g = p->groups[gids[c]];
     double w = 0.0;
-    for (const NsOp& op : chains[gi]) {
+    for (const NsOp& op : chains[c]) {
       const double tm = static_cast<double>(g.S / kTile);
       const double tiles = op.kind == OP_APPLY ? tm * static_cast<double>(g.L / kTile) : tm * (tm + 1) / 2;
       w += tiles * static_cast<double>(op.kind == OP_GRAM ? g.L : g.S);
@@ -818,7 +906,7 @@ meq_status enqueue_chains(meq_plan* p, char* ws, const std::vector<std::vector<N
   for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int>(i);
   std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return chain_work(x) > chain_work(y); });
   std::vector<Bundle> seq;
-  for (int gi : order) seq = merge_launches(seq, bundles_of(gi, chains[gi]));
+  for (int c : order) seq = merge_launches(seq, bundles_of(gids[c], chains[c]));
   for (Bundle& launch : seq) {
     std::stable_sort(launch.ops.begin(), launch.ops.end(), [&](const auto& x, const auto& y) {
       const GroupInfo& gx = p->groups[x.first];
@@ -848,19 +936,21 @@ meq_status enqueue_chains(meq_plan* p, char* ws, const std::vector<std::vector<N
 // Step a3 of a full step: every group over its own schedule, X_0 in buffer a, the prescale
 // folded into the first products; with `rowcol` the last X product also writes the row/column
 // sums of squares of its output (step a4's partials).
-meq_status enqueue_ns(meq_plan* p, char* ws, bool rowcol, hipStream_t st) {
+meq_status enqueue_ns(meq_plan* p, const Pass& ps, char* ws, bool rowcol, hipStream_t st) {
   std::vector<std::vector<NsOp>> chains;
-  for (const GroupInfo& g : p->groups) chains.push_back(group_ops(g, g.segs, true, true, rowcol, p->hp, p->gram16));
-  return enqueue_chains(p, ws, chains, st);
+  for (int gi : ps.groups) {
+    const GroupInfo& g = p->groups[gi];
+    chains.push_back(group_ops(g, g.segs, true, true, rowcol, p->hp, p->gram16));
+  }
+  return enqueue_chains(p, ws, ps.groups, chains, st);
 }
 
 // One step k of eq. "ns" as printed for every group (the CV trace replays the iterates one by
 // one): iteration k reads buffer a when k is even.
-meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, hipStream_t st) {
+meq_status enqueue_ns_iteration(meq_plan* p, const Pass& ps, char* ws, int k, hipStream_t st) {
   std::vector<std::vector<NsOp>> chains;
-  for (const GroupInfo& g : p->groups)
-    chains.push_back(group_ops(g, {1}, k % 2 == 0, k == 0, false, p->hp, p->gram16));
-  return enqueue_chains(p, ws, chains, st);
+  for (int gi : ps.groups) chains.push_back(group_ops(p->groups[gi], {1}, k % 2 == 0, k == 0, false, p->hp, p->gram16));
+  return enqueue_chains(p, ws, ps.groups, chains, st);
 }
 
 // Steps a4-a5 on the Newton-Schulz output: row/column RMS, CVs, direction and scale vectors;
@@ -868,14 +958,13 @@ meq_status enqueue_ns_iteration(meq_plan* p, char* ws, int k, hipStream_t st) {
 // squares were already written by the last X product.  The output sits where each group's
 // schedule left it, or, for the CV trace's replayed iterates, in buffer b when trace_in_b > 0
 // and a when it is 0.
-meq_status enqueue_stats(meq_plan* p, char* ws, bool moonlight, bool sums_done, hipStream_t st,
+meq_status enqueue_stats(meq_plan* p, const Pass& ps, char* ws, bool moonlight, bool sums_done, hipStream_t st,
                          int trace_in_b = -1) {
   const meq_hparams& hp = p->hp;
-  const int count = static_cast<int>(p->mats.size());
   MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
   // 4. row / column sums of squares of U, per shape group (MeqMuon only)
-  for (size_t gi = 0; gi < p->groups.size() && !moonlight && !sums_done; ++gi) {
-    const GroupInfo& g = p->groups[gi];
+  for (size_t q = 0; q < ps.groups.size() && !moonlight && !sums_done; ++q) {
+    const GroupInfo& g = p->groups[ps.groups[q]];
     const int batch = static_cast<int>(g.mats.size());
     const int tm = static_cast<int>(g.S / kTile), tn = static_cast<int>(g.L / kTile);
     uint16_t* xa = reinterpret_cast<uint16_t*>(ws + g.off_xa);
@@ -894,12 +983,12 @@ meq_status enqueue_stats(meq_plan* p, char* ws, bool moonlight, bool sums_done, 
     MEQ_TRY(timed_launch(p, MEQ_K_ROWCOL, st, [&] { return launch_rowcol(rc, batch, st); }));
   }
   // 5. row/column RMS, CVs, direction, scale vectors (Moonlight: the uniform scale)
-  for (int c0 = 0; c0 < count; c0 += kMaxChunk) {
+  for (const auto& ch : plain_chunks(ps.mats)) {
     SelectArgs a{};
-    a.count = std::min(kMaxChunk, count - c0);
+    a.count = static_cast<int>(ch.size());
     a.delta = static_cast<double>(hp.zero_rms_delta);
     for (int k = 0; k < a.count; ++k) {
-      const MatInfo& mi = p->mats[c0 + k];
+      const MatInfo& mi = p->mats[ch[k]];
       const GroupInfo& g = p->groups[mi.group];
       a.m[k] = static_cast<int>(mi.m);
       a.n[k] = static_cast<int>(mi.n);
@@ -911,7 +1000,7 @@ meq_status enqueue_stats(meq_plan* p, char* ws, bool moonlight, bool sums_done, 
       a.rrms[k] = reinterpret_cast<double*>(ws + mi.off_rrms);
       a.crms[k] = reinterpret_cast<double*>(ws + mi.off_crms);
       a.scale[k] = reinterpret_cast<float*>(ws + mi.off_scale);
-      a.scal[k] = scal + c0 + k;
+      a.scal[k] = scal + ch[k];
       a.max_lines = std::max(a.max_lines, static_cast<int>(mi.s + mi.l));
     }
     if (moonlight) {
@@ -926,10 +1015,10 @@ meq_status enqueue_stats(meq_plan* p, char* ws, bool moonlight, bool sums_done, 
 }
 
 // Step a6: decoupled weight decay and the normalized update.
-meq_status enqueue_update(meq_plan* p, char* ws, void* const* params, float lr, hipStream_t st) {
+meq_status enqueue_update(meq_plan* p, const Pass& ps, char* ws, void* const* params, float lr, hipStream_t st) {
   const meq_hparams& hp = p->hp;
   MatScalars* scal = reinterpret_cast<MatScalars*>(ws + p->off_scal);
-  const auto chunks = dtype_chunks(p);
+  const auto chunks = dtype_chunks(p, ps.mats);
   // 6. write-back
   const float decay = static_cast<float>(1.0 - static_cast<double>(lr) * hp.weight_decay);
   const float stepc = static_cast<float>(static_cast<double>(hp.rho) * lr);
@@ -983,10 +1072,12 @@ MEQ_EXPORT meq_status meq_step(meq_plan* p, void* const* params, const void* con
     if (p->kind == MEQ_PARAM_VECTOR) return step_vec(p, params, grads, momenta, lr, ws, st);
     const meq_hparams& hp = p->hp;
     const bool moonlight = hp.update_rule == MEQ_RULE_MOONLIGHT;
-    MEQ_TRY(enqueue_prescale(p, ws, grads, momenta, st));
-    MEQ_TRY(enqueue_ns(p, ws, !moonlight, st));
-    MEQ_TRY(enqueue_stats(p, ws, moonlight, !moonlight, st));
-    MEQ_TRY(enqueue_update(p, ws, params, lr, st));
+    for (const Pass& ps : p->passes) {
+      MEQ_TRY(enqueue_prescale(p, ps, ws, grads, momenta, st));
+      MEQ_TRY(enqueue_ns(p, ps, ws, !moonlight, st));
+      MEQ_TRY(enqueue_stats(p, ps, ws, moonlight, !moonlight, st));
+      MEQ_TRY(enqueue_update(p, ps, ws, params, lr, st));
+    }
     return MEQ_OK;
   });
 }
@@ -1005,17 +1096,19 @@ MEQ_EXPORT meq_status meq_ns_cv_trace(meq_plan* p, const void* const* inputs, in
   return guarded([&]() -> meq_status {
     std::vector<MatScalars> host(count);
     const char* src = ws + p->off_scal;
-    MEQ_TRY(enqueue_prescale(p, ws, inputs, nullptr, st));
-    for (int k = 0; k <= kmax; ++k) {
-      if (k > 0) MEQ_TRY(enqueue_ns_iteration(p, ws, k - 1, st));
-      // X_0 (unscaled V: CVs are scale free) sits in buffer a; iteration k - 1 writes b for odd k
-      MEQ_TRY(enqueue_stats(p, ws, false, false, st, k % 2 == 1));
-      if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
-        return MEQ_ERR_HIP;
-      if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;
-      for (int i = 0; i < count; ++i) {
-        gamma_r[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_r;
-        gamma_c[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_c;
+    for (const Pass& ps : p->passes) {
+      MEQ_TRY(enqueue_prescale(p, ps, ws, inputs, nullptr, st));
+      for (int k = 0; k <= kmax; ++k) {
+        if (k > 0) MEQ_TRY(enqueue_ns_iteration(p, ps, ws, k - 1, st));
+        // X_0 (unscaled V: CVs are scale free) sits in buffer a; iteration k - 1 writes b for odd k
+        MEQ_TRY(enqueue_stats(p, ps, ws, false, false, st, k % 2 == 1));
+        if (hipMemcpyAsync(host.data(), src, sizeof(MatScalars) * count, hipMemcpyDeviceToHost, st) != hipSuccess)
+          return MEQ_ERR_HIP;
+        if (hipStreamSynchronize(st) != hipSuccess) return MEQ_ERR_HIP;
+        for (int i : ps.mats) {
+          gamma_r[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_r;
+          gamma_c[static_cast<size_t>(i) * (kmax + 1) + k] = host[i].gamma_c;
+        }
       }
     }
     return MEQ_OK;

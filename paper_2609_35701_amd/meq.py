@@ -24,9 +24,10 @@ BUF_X0, BUF_U, BUF_NORMSQ, BUF_ROW_RMS, BUF_COL_RMS, BUF_SCALE = range(6)
 KERNEL_NAMES = ("momentum", "norm", "gram", "poly", "apply", "rowcol", "select", "update",
                 "aux_rows", "aux_cols", "aux_update", "vector")
 
-EXPORTED = ("meq_default_hparams", "meq_init", "meq_init_kind", "meq_workspace_bytes", "meq_step",
-            "meq_get_stats", "meq_ns_cv_trace", "meq_destroy", "meq_status_string", "meq_plan_num_groups", "meq_plan_group",
-            "meq_plan_group_schedule", "meq_debug_region", "meq_set_timing", "meq_get_timing")
+EXPORTED = ("meq_default_hparams", "meq_init", "meq_init_kind", "meq_init_capped", "meq_workspace_bytes", "meq_step",
+            "meq_get_stats", "meq_ns_cv_trace", "meq_destroy", "meq_status_string", "meq_plan_num_groups",
+            "meq_plan_num_passes", "meq_plan_group", "meq_plan_group_schedule", "meq_debug_region", "meq_set_timing",
+            "meq_get_timing")
 
 
 class MeqLibraryMissing(RuntimeError):
@@ -68,6 +69,9 @@ def lib() -> ctypes.CDLL:
     L.meq_init.restype = c_i32
     L.meq_init_kind.argtypes = [c_i32, ctypes.POINTER(MatrixDesc), c_i32, ctypes.POINTER(HParams), ctypes.POINTER(vp)]
     L.meq_init_kind.restype = c_i32
+    L.meq_init_capped.argtypes = [c_i32, ctypes.POINTER(MatrixDesc), c_i32, ctypes.POINTER(HParams), c_sz,
+                                  ctypes.POINTER(vp)]
+    L.meq_init_capped.restype = c_i32
     L.meq_workspace_bytes.argtypes = [vp]
     L.meq_workspace_bytes.restype = c_sz
     L.meq_step.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.c_float, vp,
@@ -85,6 +89,8 @@ def lib() -> ctypes.CDLL:
     L.meq_status_string.restype = ctypes.c_char_p
     L.meq_plan_num_groups.argtypes = [vp]
     L.meq_plan_num_groups.restype = c_i32
+    L.meq_plan_num_passes.argtypes = [vp]
+    L.meq_plan_num_passes.restype = c_i32
     L.meq_plan_group.argtypes = [vp, c_i32, ctypes.POINTER(c_i64), ctypes.POINTER(c_i64), ctypes.POINTER(c_i32)]
     L.meq_plan_group.restype = c_i32
     L.meq_plan_group_schedule.argtypes = [vp, c_i32, ctypes.POINTER(c_i32), c_i32, ctypes.POINTER(c_i32)]
@@ -129,13 +135,14 @@ def _dtype_code(dtype) -> int:
 
 
 class Plan:
-    """A validated set of parameters of one kind plus hyperparameters (``meq_init_kind``).
+    """A validated set of parameters of one kind plus hyperparameters (``meq_init_capped``).
 
     ``kind`` is PARAM_HIDDEN (2D hidden weights), PARAM_AUX (remaining 2D parameters)
-    or PARAM_VECTOR (1-D parameters; a shape (1, d) or (d,) each)."""
+    or PARAM_VECTOR (1-D parameters; a shape (1, d) or (d,) each).  ``max_workspace_bytes``
+    caps the plan's workspace (0: no cap)."""
 
     def __init__(self, shapes: Sequence[Tuple[int, ...]], param_dtype="bf16", grad_dtype=None,
-                 hparams: Optional[HParams] = None, kind: int = PARAM_HIDDEN):
+                 hparams: Optional[HParams] = None, kind: int = PARAM_HIDDEN, max_workspace_bytes: int = 0):
         L = lib()
         self.kind = int(kind)
         self.shapes = [(1, int(sh[0])) if len(sh) == 1 else (int(sh[0]), int(sh[1])) for sh in shapes]
@@ -147,8 +154,8 @@ class Plan:
             descs[i] = MatrixDesc(r, c, pd, gd)
         self.hparams = hparams if hparams is not None else default_hparams()
         handle = ctypes.c_void_p()
-        _check(L.meq_init_kind(self.kind, descs, n, ctypes.byref(self.hparams), ctypes.byref(handle)),
-               "meq_init_kind")
+        _check(L.meq_init_capped(self.kind, descs, n, ctypes.byref(self.hparams), ctypes.c_size_t(max_workspace_bytes),
+                                 ctypes.byref(handle)), "meq_init_capped")
         self._h = handle
         self.count = n
 
@@ -165,6 +172,10 @@ class Plan:
     @property
     def workspace_bytes(self) -> int:
         return int(lib().meq_workspace_bytes(self._h))
+
+    @property
+    def passes(self) -> int:
+        return int(lib().meq_plan_num_passes(self._h))
 
     def groups(self) -> List[Tuple[int, int, int]]:
         L = lib()
@@ -245,7 +256,8 @@ class ParamUpdate:
 
     kind = PARAM_HIDDEN
 
-    def __init__(self, params, hparams: Optional[HParams] = None, kind: Optional[int] = None):
+    def __init__(self, params, hparams: Optional[HParams] = None, kind: Optional[int] = None,
+                 max_workspace_bytes: int = 0):
         import torch
 
         if kind is not None:
@@ -261,7 +273,7 @@ class ParamUpdate:
             if self.kind != PARAM_VECTOR and p.dim() != 2:
                 raise ValueError("hidden and aux parameters must be 2D")
         shapes = [tuple(p.shape) if self.kind != PARAM_VECTOR else (p.numel(),) for p in self.params]
-        self.plan = Plan(shapes, str(pdt), hparams=hparams, kind=self.kind)
+        self.plan = Plan(shapes, str(pdt), hparams=hparams, kind=self.kind, max_workspace_bytes=max_workspace_bytes)
         self.momenta = [torch.zeros(p.shape, dtype=torch.float32, device=dev) for p in self.params]
         self.workspace = torch.empty(max(self.plan.workspace_bytes, 256), dtype=torch.uint8, device=dev)
 

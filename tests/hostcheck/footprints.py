@@ -34,6 +34,11 @@ def load(path: str) -> ctypes.CDLL:
     L.meq_init_kind.argtypes = [i32, ctypes.POINTER(meq.MatrixDesc), i32, ctypes.POINTER(meq.HParams),
                                 ctypes.POINTER(vp)]
     L.meq_init_kind.restype = i32
+    L.meq_init_capped.argtypes = [i32, ctypes.POINTER(meq.MatrixDesc), i32, ctypes.POINTER(meq.HParams), sz,
+                                  ctypes.POINTER(vp)]
+    L.meq_init_capped.restype = i32
+    L.meq_plan_num_passes.argtypes = [vp]
+    L.meq_plan_num_passes.restype = i32
     L.meq_workspace_bytes.argtypes = [vp]
     L.meq_workspace_bytes.restype = sz
     L.meq_step.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.c_float, vp, sz, vp]
@@ -104,17 +109,21 @@ def _covered(merged, lo, hi) -> bool:
     return i >= 0 and merged[i][0] <= lo and hi <= merged[i][1]
 
 
-def record_step(L, kind: int, shapes: Sequence[Tuple[int, int]], dtype: str = "bf16", **hp_over) -> dict:
-    """Build a plan in the host-check library and record one meq_step with fake device addresses."""
+def record_step(L, kind: int, shapes: Sequence[Tuple[int, int]], dtype: str = "bf16", max_ws: int = 0,
+                **hp_over) -> dict:
+    """Build a plan in the host-check library (workspace capped at max_ws bytes unless 0) and record
+    one meq_step with fake device addresses."""
     dt = meq.MEQ_BF16 if dtype == "bf16" else meq.MEQ_F32
     n = len(shapes)
     descs = (meq.MatrixDesc * max(n, 1))(*[meq.MatrixDesc(r, c, dt, dt) for r, c in shapes])
     hp = _hparams(L, **hp_over)
     h = ctypes.c_void_p()
-    st = L.meq_init_kind(kind, descs, n, ctypes.byref(hp), ctypes.byref(h))
+    st = L.meq_init_capped(kind, descs, n, ctypes.byref(hp), max_ws, ctypes.byref(h))
     assert st == meq.MEQ_OK, f"init {st}"
     try:
         ws_bytes = L.meq_workspace_bytes(h)
+        passes = L.meq_plan_num_passes(h)
+        assert max_ws == 0 or ws_bytes <= max_ws, f"workspace {ws_bytes} above the cap {max_ws}"
         params = (ctypes.c_void_p * n)(*[PARAM_BASE + i * SLOT for i in range(n)])
         grads = (ctypes.c_void_p * n)(*[GRAD_BASE + i * SLOT for i in range(n)])
         moms = (ctypes.c_void_p * n)(*[MOM_BASE + i * SLOT for i in range(n)])
@@ -122,6 +131,7 @@ def record_step(L, kind: int, shapes: Sequence[Tuple[int, int]], dtype: str = "b
         st = L.meq_step(h, params, grads, moms, ctypes.c_float(0.02), ctypes.c_void_p(WS_BASE), ws_bytes, None)
         assert st == meq.MEQ_OK, f"step {st}"
         return {"kind": kind, "shapes": list(shapes), "esz": 2 if dtype == "bf16" else 4, "ws_bytes": ws_bytes,
+                "passes": passes,
                 "ranges": _ranges(L), "covers": _covers(L), "launches": L.meq_hc_num_launches()}
     finally:
         L.meq_destroy(h)
@@ -184,10 +194,17 @@ def check_record(rec: dict, label: str = "") -> dict:
         assert got == want, f"{label}: padded covers {got[:4]} vs {want[:4]}"
         for _, _, _, rows, cols, ld in covers:
             assert ld == cols, f"{label}: leading dimension {ld} of a {rows} x {cols} buffer"
+    # every matrix's parameter is written exactly once per step, whatever the passes
+    if rec["kind"] == meq.PARAM_HIDDEN:
+        wr = sorted((r[5] - PARAM_BASE) // SLOT for r in ranges if r[4] == "W" and r[2] != READ)
+        assert wr == list(range(n)), f"{label}: parameters written {wr[:8]}... for {n} matrices"
     return {"launches": launches, "ranges": len(ranges), "ws_bytes": ws_bytes}
 
 
 def check_plan(L, kind: int, shapes: Sequence[Tuple[int, int]], dtype: str = "bf16", label: str = "",
-               **hp_over) -> dict:
+               max_ws: int = 0, **hp_over) -> dict:
     """Record one step of a plan and check every launch's ranges; returns a summary."""
-    return check_record(record_step(L, kind, shapes, dtype, **hp_over), label)
+    rec = record_step(L, kind, shapes, dtype, max_ws, **hp_over)
+    out = check_record(rec, label)
+    out["passes"] = rec["passes"]
+    return out

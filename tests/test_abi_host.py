@@ -355,3 +355,34 @@ def test_split_parameters_classifies_kinds():
 
     with pytest.raises(ValueError):
         split_parameters(Conv())
+
+
+def test_capped_plans_fit_their_cap_and_split_into_passes():
+    shapes = [(m.rows, m.cols) for m in workloads.workload("llama-1b").matrices]
+    full = meq.Plan(shapes, "bf16")
+    assert full.passes == 1
+    same = meq.Plan(shapes, "bf16", max_workspace_bytes=0)
+    assert same.workspace_bytes == full.workspace_bytes and same.groups() == full.groups()
+    for cap in (4 << 30, 1 << 30, 256 << 20):
+        p = meq.Plan(shapes, "bf16", max_workspace_bytes=cap)
+        assert p.workspace_bytes <= cap and p.passes >= 2
+        # slices of the shape groups add up to the groups, each with its group's schedule
+        tot = {}
+        for g, (s_, l_, c) in enumerate(p.groups()):
+            tot[(s_, l_)] = tot.get((s_, l_), 0) + c
+            assert p.schedule(g) == full.schedule([x[:2] for x in full.groups()].index((s_, l_)))
+        assert tot == {(s_, l_): c for s_, l_, c in full.groups()}
+    # a cap above the uncapped workspace changes nothing
+    big = meq.Plan(shapes, "bf16", max_workspace_bytes=full.workspace_bytes + 4096)
+    assert big.passes == 1 and big.workspace_bytes == full.workspace_bytes
+
+
+def test_capped_plans_reject_caps_too_small():
+    for shapes, cap in (([(2048, 8192)], 64 << 20), ([(256, 512)] * 4, 4096)):
+        with pytest.raises(meq.MeqError) as e:
+            meq.Plan(shapes, "bf16", max_workspace_bytes=cap)
+        assert e.value.status == meq.MEQ_ERR_WORKSPACE
+    with pytest.raises(meq.MeqError) as e:
+        meq.Plan([(32000, 2048)], "bf16", kind=meq.PARAM_AUX, max_workspace_bytes=1024)
+    assert e.value.status == meq.MEQ_ERR_WORKSPACE
+    assert meq.Plan([(32000, 2048)], "bf16", kind=meq.PARAM_AUX, max_workspace_bytes=64 << 20).passes == 0

@@ -59,6 +59,22 @@ def test_many_matrices_span_several_launch_chunks(hc):
     footprints.check_plan(hc, meq.PARAM_HIDDEN, shapes[:140] + [(2, 3)] * 140, "f32", "280 matrices")
 
 
+@pytest.mark.parametrize("name,cap_mib", [("llama-1b", 256), ("llama-1b", 128), ("llama-130m", 64),
+                                          ("llama-7b-block-x4", 512), ("llama-350m-ffn2736", 100)])
+def test_capped_plans(hc, name, cap_mib):
+    wl = workloads.workload(name)
+    shapes = [(m.rows, m.cols) for m in wl.matrices]
+    out = footprints.check_plan(hc, meq.PARAM_HIDDEN, shapes, wl.param_dtype, f"{name} cap {cap_mib} MiB",
+                                max_ws=cap_mib << 20)
+    assert out["ws_bytes"] <= cap_mib << 20 and out["passes"] > 1
+
+
+def test_capped_odd_shapes(hc):
+    out = footprints.check_plan(hc, meq.PARAM_HIDDEN, ODD_SHAPES * 3, "f32", "odd capped", max_ws=24 << 20,
+                                ns_gram_steps=2)
+    assert out["passes"] > 1
+
+
 def test_aux_and_vector_plans(hc):
     footprints.check_plan(hc, meq.PARAM_AUX, [(32000, 2048), (300, 64), (1, 1), (7, 5)], "bf16", "aux")
     footprints.check_plan(hc, meq.PARAM_AUX, [(129, 65536), (1, 3)], "f32", "aux f32", nesterov=1)
