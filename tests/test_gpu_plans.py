@@ -64,3 +64,31 @@ def test_two_plans_interleaved_on_one_stream_match_sequential_runs():
             assert torch.equal(x.params[k], y.params[k])
             assert torch.equal(x.upd.momenta[k], y.upd.momenta[k])
         assert x.upd.stats() == y.upd.stats()
+
+
+def test_capped_plan_matches_the_uncapped_plan_bitwise():
+    """A workspace-capped plan runs its matrices in several passes that reuse one Newton-Schulz
+    region; every matrix's arithmetic is the same, so parameters, momenta and statistics match the
+    uncapped plan bit for bit over several steps (mixed shapes, tall and wide, fp32 and bf16)."""
+    from paper_2609_35701_amd import meq
+
+    for dtype, shapes, cap in (("bf16", [(m.rows, m.cols) for m in workloads.workload("llama-130m").matrices[:14]],
+                                32 << 20),
+                               ("f32", [(300, 100), (1024, 256), (256, 1024), (96, 640), (7, 5), (512, 512)],
+                                4 << 20)):
+        wl = workloads.custom(shapes, dtype, name=f"capped-{dtype}", seed=57)
+        log(f"[case] capped plan {dtype} {len(shapes)} matrices cap {cap >> 20} MiB")
+        w0 = [to_dev(workloads.weight_init(wl, i), dtype) for i in range(wl.count)]
+        ref = meq.HiddenWeightUpdate([w.clone() for w in w0])
+        cap_upd = meq.HiddenWeightUpdate([w.clone() for w in w0], max_workspace_bytes=cap)
+        assert cap_upd.plan.passes >= 3 and cap_upd.plan.workspace_bytes <= cap
+        assert ref.plan.passes == 1
+        for s in range(3):
+            g = [to_dev(workloads.grad_at_step(wl, i, s), dtype) for i in range(wl.count)]
+            ref.step(g, 0.02)
+            cap_upd.step(g, 0.02)
+        torch.cuda.synchronize()
+        for k in range(wl.count):
+            assert torch.equal(ref.params[k], cap_upd.params[k]), f"{dtype}: parameter {k}"
+            assert torch.equal(ref.momenta[k], cap_upd.momenta[k]), f"{dtype}: momentum {k}"
+        assert ref.stats() == cap_upd.stats()
