@@ -226,6 +226,29 @@ meq_status meq_get_stats(const meq_plan* plan, const void* workspace, double* ga
 meq_status meq_ns_cv_trace(meq_plan* plan, const void* const* inputs, int32_t kmax, void* workspace,
                            size_t workspace_bytes, double* gamma_r, double* gamma_c, hipStream_t stream);
 
+/*
+ * Bytes of the device scratch array meq_step_static uses as its workspace: one array per GPU the
+ * library runs on, allocated with the library's code object and held until the process ends.
+ */
+#define MEQ_STATIC_SCRATCH_BYTES ((size_t)256 << 20)
+
+/*
+ * meq_step without a caller workspace, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  Same
+ * arguments and update as meq_step; the workspace is the library's scratch array on the current
+ * device (the stream must belong to the current device).  Nothing is allocated or freed: no
+ * hipMalloc, hipFree or allocating library routine is called, only hipGetDevice and, once per
+ * device, hipGetSymbolAddress.  A plan whose meq_workspace_bytes exceeds
+ * MEQ_STATIC_SCRATCH_BYTES is rejected with MEQ_ERR_WORKSPACE before any device work; build such
+ * plans with meq_init_capped(..., MEQ_STATIC_SCRATCH_BYTES, ...).  Every call on one GPU shares
+ * that GPU's array and leaves its contents behind (nothing in it needs to start at zero: a step
+ * writes every workspace byte it reads); calls that overlap on one GPU, on any streams or plans,
+ * race on it and must be serialized by the caller.  The statistics meq_get_stats reads stay in
+ * the library's array, so they are not available after this variant.
+ */
+meq_status meq_step_static(meq_plan* plan, void* const* params, const void* const* grads, float* const* momenta,
+                           float lr, hipStream_t stream);
+
 /* Release a plan (null is a no-op).  Pending timing events are destroyed. */
 void meq_destroy(meq_plan* plan);
 

@@ -27,6 +27,7 @@ SOURCES = {
     "k_stream.hip": [],
     "k_aux.hip": [],
     "meq_api.cpp": [],
+    "meq_static.hip": [],
 }
 
 

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(HERE, "libmeq.so")
 
 MEQ_OK, MEQ_ERR_INVALID_ARG, MEQ_ERR_UNSUPPORTED, MEQ_ERR_HIP, MEQ_ERR_WORKSPACE, MEQ_ERR_NO_MEMORY = 0, -1, -2, -3, -4, -5
 MEQ_F32, MEQ_BF16 = 0, 1
+MEQ_STATIC_SCRATCH_BYTES = 256 << 20
 MEQ_DIR_ROW, MEQ_DIR_COL = 0, 1
 PARAM_HIDDEN, PARAM_AUX, PARAM_VECTOR = 0, 1, 2
 RULE_MEQMUON, RULE_MOONLIGHT = 0, 1
@@ -27,7 +28,7 @@ KERNEL_NAMES = ("momentum", "norm", "gram", "poly", "apply", "rowcol", "select",
 EXPORTED = ("meq_default_hparams", "meq_init", "meq_init_kind", "meq_init_capped", "meq_workspace_bytes", "meq_step",
             "meq_get_stats", "meq_ns_cv_trace", "meq_destroy", "meq_status_string", "meq_plan_num_groups",
             "meq_plan_num_passes", "meq_plan_group", "meq_plan_group_schedule", "meq_debug_region", "meq_set_timing",
-            "meq_get_timing")
+            "meq_get_timing", "meq_step_static")
 
 
 class MeqLibraryMissing(RuntimeError):
@@ -77,6 +78,8 @@ def lib() -> ctypes.CDLL:
     L.meq_step.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.c_float, vp,
                            c_sz, vp]
     L.meq_step.restype = c_i32
+    L.meq_step_static.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.c_float, vp]
+    L.meq_step_static.restype = c_i32
     L.meq_get_stats.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                 ctypes.POINTER(c_i32), vp]
     L.meq_get_stats.restype = c_i32
@@ -211,6 +214,15 @@ class Plan:
         B = (ctypes.c_void_p * max(n, 1))(*moms)
         _check(lib().meq_step(self._h, P, G, B, ctypes.c_float(lr), ctypes.c_void_p(workspace),
                               ctypes.c_size_t(workspace_bytes), ctypes.c_void_p(stream)), "meq_step")
+
+    def step_static_ptrs(self, params: Sequence[int], grads: Sequence[int], moms: Sequence[int], lr: float,
+                         stream: int = 0) -> None:
+        """``meq_step_static`` (the library's own scratch as the workspace) on raw device addresses."""
+        n = self.count
+        P = (ctypes.c_void_p * max(n, 1))(*params)
+        G = (ctypes.c_void_p * max(n, 1))(*grads)
+        B = (ctypes.c_void_p * max(n, 1))(*moms)
+        _check(lib().meq_step_static(self._h, P, G, B, ctypes.c_float(lr), ctypes.c_void_p(stream)), "meq_step_static")
 
     def stats_ptr(self, workspace: int, stream: int = 0):
         n = self.count

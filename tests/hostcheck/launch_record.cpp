@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <vector>
 
+#include "meq.h"
 #include "meq_internal.h"
 
 #define HC_EXPORT extern "C" __attribute__((visibility("default")))
@@ -250,6 +251,20 @@ hipError_t launch_vec(const VecArgs& a, int bf16, hipStream_t) {
 }
 
 }  // namespace meq
+
+// The no-allocation step: the library's version takes its workspace from a device array; here the
+// array is a fake address range past the other fake buffers, checked like any workspace.
+constexpr uintptr_t kFakeScratch = uintptr_t{5} << 44;
+
+HC_EXPORT meq_status meq_step_static(meq_plan* plan, void* const* params, const void* const* grads,
+                                     float* const* momenta, float lr, hipStream_t stream) {
+  if (!plan) return MEQ_ERR_INVALID_ARG;
+  const size_t need = meq_workspace_bytes(plan);
+  if (need > MEQ_STATIC_SCRATCH_BYTES) return MEQ_ERR_WORKSPACE;
+  if (need == 0) return meq_step(plan, params, grads, momenta, lr, nullptr, 0, stream);
+  return meq_step(plan, params, grads, momenta, lr, reinterpret_cast<void*>(kFakeScratch), MEQ_STATIC_SCRATCH_BYTES,
+                  stream);
+}
 
 // ------------------------------------------------------------------ queries for the tests
 HC_EXPORT void meq_hc_clear(void) {

@@ -386,3 +386,19 @@ def test_capped_plans_reject_caps_too_small():
         meq.Plan([(32000, 2048)], "bf16", kind=meq.PARAM_AUX, max_workspace_bytes=1024)
     assert e.value.status == meq.MEQ_ERR_WORKSPACE
     assert meq.Plan([(32000, 2048)], "bf16", kind=meq.PARAM_AUX, max_workspace_bytes=64 << 20).passes == 0
+
+
+def test_step_static_rejects_plans_beyond_its_scratch_before_any_device_work():
+    L = meq.lib()
+    assert meq.MEQ_STATIC_SCRATCH_BYTES == 256 << 20
+    header = open(os.path.join(ROOT, "include", "meq.h")).read()
+    assert "#define MEQ_STATIC_SCRATCH_BYTES ((size_t)256 << 20)" in header
+    big = meq.Plan([(m.rows, m.cols) for m in workloads.workload("llama-1b").matrices], "bf16")
+    assert big.workspace_bytes > meq.MEQ_STATIC_SCRATCH_BYTES
+    n = big.count
+    ptrs = (ctypes.c_void_p * n)(*([0x1000] * n))
+    assert L.meq_step_static(big.handle, ptrs, ptrs, ptrs, ctypes.c_float(0.02), None) == meq.MEQ_ERR_WORKSPACE
+    assert L.meq_step_static(None, ptrs, ptrs, ptrs, ctypes.c_float(0.02), None) == meq.MEQ_ERR_INVALID_ARG
+    capped = meq.Plan([(m.rows, m.cols) for m in workloads.workload("llama-1b").matrices], "bf16",
+                      max_workspace_bytes=meq.MEQ_STATIC_SCRATCH_BYTES)
+    assert capped.workspace_bytes <= meq.MEQ_STATIC_SCRATCH_BYTES
