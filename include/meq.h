@@ -30,6 +30,12 @@
  *   - Functions that return meq_status validate every argument before any
  *     device work; on an argument error nothing is enqueued and no caller
  *     memory is modified.  HIP failures are reported as MEQ_ERR_HIP.
+ *   - A step enqueues many kernels.  When a launch fails part-way (MEQ_ERR_HIP,
+ *     MEQ_ERR_NO_MEMORY or MEQ_ERR_INTERNAL from meq_step), the launches before
+ *     it stay enqueued and the ones after it are not: some matrices may have
+ *     their momenta (and, for a later pass or kernel, parameters) updated while
+ *     others do not.  The step is not atomic; a caller that must recover keeps a
+ *     copy of the parameters and momenta.
  *   - No entry point blocks the host except meq_get_stats, meq_ns_cv_trace and
  *     meq_get_timing, which synchronize with the given stream.
  *   - A plan is not reentrant: do not run two meq_step calls of one plan (or
@@ -53,8 +59,10 @@ typedef enum {
   MEQ_ERR_UNSUPPORTED = -2, /* a dtype combination or size the library does not implement        */
   MEQ_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed                          */
   MEQ_ERR_WORKSPACE = -4,   /* the workspace is null, too small or not 256-byte aligned           */
-  MEQ_ERR_NO_MEMORY = -5    /* a host allocation (plan metadata, launch lists) failed; no launch   */
+  MEQ_ERR_NO_MEMORY = -5,   /* a host allocation (plan metadata, launch lists) failed; no launch   */
                             /* of the failing call was enqueued after the failure                  */
+  MEQ_ERR_INTERNAL = -6     /* an unexpected host-side failure inside the library (a bug); no      */
+                            /* launch of the failing call was enqueued after it                    */
 } meq_status;
 
 typedef enum { MEQ_F32 = 0, MEQ_BF16 = 1 } meq_dtype;

@@ -212,7 +212,7 @@ meq_status guarded(F&& fn) {
   } catch (const std::bad_alloc&) {
     return MEQ_ERR_NO_MEMORY;
   } catch (...) {
-    return MEQ_ERR_INVALID_ARG;
+    return MEQ_ERR_INTERNAL;
   }
 }
 
@@ -242,6 +242,7 @@ MEQ_EXPORT const char* meq_status_string(meq_status s) {
     case MEQ_ERR_HIP: return "HIP runtime error";
     case MEQ_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
     case MEQ_ERR_NO_MEMORY: return "host memory allocation failed";
+    case MEQ_ERR_INTERNAL: return "internal library error";
   }
   return "unknown status";
 }

@@ -13,7 +13,8 @@ from typing import Iterable, List, Optional, Sequence, Tuple
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmeq.so")
 
-MEQ_OK, MEQ_ERR_INVALID_ARG, MEQ_ERR_UNSUPPORTED, MEQ_ERR_HIP, MEQ_ERR_WORKSPACE, MEQ_ERR_NO_MEMORY = 0, -1, -2, -3, -4, -5
+(MEQ_OK, MEQ_ERR_INVALID_ARG, MEQ_ERR_UNSUPPORTED, MEQ_ERR_HIP, MEQ_ERR_WORKSPACE, MEQ_ERR_NO_MEMORY,
+ MEQ_ERR_INTERNAL) = 0, -1, -2, -3, -4, -5, -6
 MEQ_F32, MEQ_BF16 = 0, 1
 MEQ_STATIC_SCRATCH_BYTES = 256 << 20
 MEQ_DIR_ROW, MEQ_DIR_COL = 0, 1

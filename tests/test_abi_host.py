@@ -38,11 +38,11 @@ def test_default_hparams_are_the_papers():
 def test_status_strings_cover_every_status():
     header = open(os.path.join(ROOT, "include", "meq.h")).read()
     codes = {int(v) for v in re.findall(r"MEQ_(?:OK|ERR_[A-Z_]+) = (-?\d+)", header)}
-    assert codes == {0, -1, -2, -3, -4, -5}
+    assert codes == {0, -1, -2, -3, -4, -5, -6}
     texts = {meq.status_string(c) for c in codes}
     assert len(texts) == len(codes) and "unknown status" not in texts
     assert meq.status_string(-99) == "unknown status"
-    assert meq.MEQ_ERR_NO_MEMORY == -5
+    assert meq.MEQ_ERR_NO_MEMORY == -5 and meq.MEQ_ERR_INTERNAL == -6
 
 
 def _init(descs, hp=None):
