@@ -52,3 +52,43 @@ def test_static_step_rejects_a_plan_beyond_its_scratch():
     with pytest.raises(meq.MeqError) as e:
         plan.step_static_ptrs([x.data_ptr()] * 7, [x.data_ptr()] * 7, [x.data_ptr()] * 7, 0.02)
     assert e.value.status == meq.MEQ_ERR_WORKSPACE
+
+
+def test_static_step_captured_in_a_graph_replays_like_the_workspace_step():
+    """The point of the entry point: a step that allocates nothing can be captured into a HIP graph
+    and replayed; each replay equals the eager workspace step bitwise."""
+    shapes = [(256, 1024), (1024, 256), (300, 100)]
+    wl = workloads.custom(shapes, "bf16", name="noalloc-graph", seed=75)
+    w0 = [to_dev(workloads.weight_init(wl, i), "bf16") for i in range(wl.count)]
+    grads = [[to_dev(workloads.grad_at_step(wl, i, s), "bf16") for i in range(wl.count)] for s in range(3)]
+    log("[case] no-alloc step in a graph: 3 replays")
+    # the device's scratch address is looked up on a first eager call, outside the capture
+    warm = meq.Plan([(7, 5)], "bf16")
+    x = [torch.zeros(7, 5, dtype=torch.bfloat16, device="cuda:0")]
+    xb = [torch.zeros(7, 5, dtype=torch.float32, device="cuda:0")]
+    warm.step_static_ptrs([x[0].data_ptr()], [x[0].data_ptr()], [xb[0].data_ptr()], 0.0,
+                          torch.cuda.current_stream().cuda_stream)
+    ref = meq.HiddenWeightUpdate([w.clone() for w in w0])
+    plan = meq.Plan(shapes, "bf16")
+    params = [w.clone() for w in w0]
+    moms = [torch.zeros(w.shape, dtype=torch.float32, device=w.device) for w in w0]
+    static_g = [torch.zeros_like(g) for g in grads[0]]
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        plan.step_static_ptrs([p.data_ptr() for p in params], [g.data_ptr() for g in static_g],
+                              [b.data_ptr() for b in moms], 0.02, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    for p, w in zip(params, w0):
+        assert torch.equal(p, w), "capture must not run the step"
+    for s in range(3):
+        ref.step(grads[s], 0.02)
+        for dst, src in zip(static_g, grads[s]):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k in range(len(shapes)):
+            assert torch.equal(params[k], ref.params[k]), f"replay {s}: parameter {k}"
+            assert torch.equal(moms[k], ref.momenta[k]), f"replay {s}: momentum {k}"
+    graph.reset()
