@@ -339,7 +339,14 @@ def extras_leg(params, wl, lr: float, steps: int, warmup: int) -> dict:
     literal = meq.HiddenWeightUpdate(params, meq.default_hparams(ns_gram_steps=1))
     out["printed_iteration_hidden"] = time_steps(literal, g_hidden, lr, steps, warmup,
                                                  [meq.K_GRAM, meq.K_POLY, meq.K_APPLY])
-    del moon, literal, g_hidden
+    del moon, literal
+    # the same step with the workspace capped to the static scratch size: passes that reuse one
+    # Newton-Schulz region (what a caller without a large workspace, or meq_step_static, runs)
+    capped = meq.HiddenWeightUpdate(params, max_workspace_bytes=meq.MEQ_STATIC_SCRATCH_BYTES)
+    out["capped_workspace_hidden"] = time_steps(capped, g_hidden, lr, steps, warmup, [meq.K_APPLY])
+    out["capped_workspace_hidden"].update({"workspace_bytes": capped.plan.workspace_bytes,
+                                           "passes": capped.plan.passes})
+    del capped, g_hidden
     torch.cuda.empty_cache()
     # remaining 2D parameters: the Llama token embedding and LM head (32000 x 2048, untied), bf16
     aux_p = [torch.randn(32000, 2048, device=dev).mul_(0.02).to(torch.bfloat16) for _ in range(2)]

@@ -92,3 +92,29 @@ def test_capped_plan_matches_the_uncapped_plan_bitwise():
             assert torch.equal(ref.params[k], cap_upd.params[k]), f"{dtype}: parameter {k}"
             assert torch.equal(ref.momenta[k], cap_upd.momenta[k]), f"{dtype}: momentum {k}"
         assert ref.stats() == cap_upd.stats()
+
+
+def test_capped_1b_plan_at_full_size_matches_uncapped_and_static_step():
+    """The 1B-shape step (112 matrices) capped to the static scratch size runs in 30 passes; with a
+    caller workspace and through meq_step_static it matches the uncapped step bit for bit."""
+    from paper_2609_35701_amd import meq
+
+    wl = workloads.workload("llama-1b")
+    log(f"[case] llama-1b capped to {meq.MEQ_STATIC_SCRATCH_BYTES >> 20} MiB against uncapped")
+    params, grads, _ = workloads.device_inputs(wl, "cuda:0")
+    ref = meq.HiddenWeightUpdate([p.clone() for p in params])
+    cap = meq.HiddenWeightUpdate([p.clone() for p in params], max_workspace_bytes=meq.MEQ_STATIC_SCRATCH_BYTES)
+    assert cap.plan.passes >= 20 and cap.plan.workspace_bytes <= meq.MEQ_STATIC_SCRATCH_BYTES
+    static_plan = meq.Plan([tuple(p.shape) for p in params], "bf16", max_workspace_bytes=meq.MEQ_STATIC_SCRATCH_BYTES)
+    sp = [p.clone() for p in params]
+    sb = [torch.zeros(p.shape, dtype=torch.float32, device=p.device) for p in params]
+    for _ in range(2):
+        ref.step(grads, 0.02)
+        cap.step(grads, 0.02)
+        static_plan.step_static_ptrs([p.data_ptr() for p in sp], [g.data_ptr() for g in grads],
+                                     [b.data_ptr() for b in sb], 0.02, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    for k in range(wl.count):
+        assert torch.equal(ref.params[k], cap.params[k]) and torch.equal(ref.params[k], sp[k]), f"parameter {k}"
+        assert torch.equal(ref.momenta[k], cap.momenta[k]) and torch.equal(ref.momenta[k], sb[k]), f"momentum {k}"
+    assert ref.stats() == cap.stats()
