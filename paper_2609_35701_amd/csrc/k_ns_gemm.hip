@@ -132,7 +132,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   constexpr int kDma = 16;             // LDS-bound buffer loads per wave per slab (8 per operand)
   // Ring buffers as separate objects, so the compiler can tell the buffer being read from
   // the buffers being filled: st0, st1 hold operand A, st2, st3, st4 operand B.  The
-  // epilogue stages its output in st0..st3 and the fused column sums in st4.
+  // epilogue stages its output in st0..st3 and the fused row and column partials in st4.
   __shared__ __attribute__((aligned(1024))) uint8_t st0_[kBufBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t st1_[kBufBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t st2_[kBufBytes];
@@ -473,6 +473,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     combine(std::true_type{});
   else
     combine(std::false_type{});
+  // x0^2 + x1^2 + acc for a packed bf16 pair (v_dot2: the bf16 products are exact in fp32)
+  auto sq2 = [](uint32_t x, float acc) {
+    const bf16x2 v = __builtin_bit_cast(bf16x2, x);
+    return __builtin_amdgcn_fdot2_f32_bf16(v, v, acc, false);
+  };
+  // apply with fused sums: per-lane row partials of the bf16 output straight from the packed
+  // registers (each lane holds 64 values of each of its 4 rows), one slot per (wn, h) half of
+  // the row, in the ring's fifth buffer behind the column partials
+  lds_f32* const rowpart = (lds_f32*)(st4_ + 8192);
+  if (kNN && g.rpart) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float rs = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int vq = 0; vq < 4; ++vq) rs = sq2(packed[i][j][vq].y, sq2(packed[i][j][vq].x, rs));
+      rowpart[256 * (2 * wn + h) + 128 * wm + 32 * i + (lane & 31)] = rs;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -532,40 +552,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
 
   if (kNN && g.rpart) {
-    // Row and column sums of squares of this bf16 output tile, read back from its staged
-    // copy in a fixed order.  Row t: its 32 16-byte chunks, thread t starting at chunk t % 32 so
-    // the 16 lanes of an LDS pass hit 16 different bank groups.  Columns: wave w sums its own
-    // stage (rows 64 w .. 64 w + 63), 4 columns per lane, and the four waves meet in LDS.
-    const lds_u8* srow = stage_of(t >> 6);
-    float rsum = 0.f;
-#pragma unroll 8
-    for (int p = 0; p < 32; ++p) {
-      const int slot = (p + t) & 31;
-      const u32x4 v = *reinterpret_cast<const lds_u32x4*>(srow + (t & 63) * 512 + 16 * slot);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float lo = bf16_to_f32(v[e] & 0xffffu), hi = bf16_to_f32(v[e] >> 16);
-        rsum = fmaf(lo, lo, rsum);
-        rsum = fmaf(hi, hi, rsum);
-      }
-    }
-    const int c4 = 4 * lane;  // columns c4 .. c4 + 3
+    // Row and column sums of squares of this bf16 output tile, in a fixed order.  Rows: the four
+    // register partials of each row.  Columns: wave w sums its own stage (rows 64 w .. 64 w + 63)
+    // with transpose reads, lane q of 16-lane group g4 taking 4 consecutive rows of column
+    // 16 (4 m + g4) + q per read, and the four waves meet in LDS.
+    const int jq16 = lane & 15, g4 = lane >> 4;
     const lds_u8* sw = stage_of(wave);
     float cs[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 16
-    for (int rr = 0; rr < 64; ++rr) {
-      const u32x2 v = *reinterpret_cast<const lds_u32x2*>(sw + stage_byte(64 * wave + rr, c4));
-      const float x0 = bf16_to_f32(v.x & 0xffffu), x1 = bf16_to_f32(v.x >> 16);
-      const float x2 = bf16_to_f32(v.y & 0xffffu), x3 = bf16_to_f32(v.y >> 16);
-      cs[0] = fmaf(x0, x0, cs[0]);
-      cs[1] = fmaf(x1, x1, cs[1]);
-      cs[2] = fmaf(x2, x2, cs[2]);
-      cs[3] = fmaf(x3, x3, cs[3]);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+#pragma unroll 4
+      for (int rb = 0; rb < 16; ++rb) {
+        const int r = 64 * wave + 4 * rb + (jq16 >> 2);
+        const int c = 16 * (4 * m + g4) + 4 * (jq16 & 3);
+        const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sw + stage_byte(r, c)));
+        const u32x2 w2 = __builtin_bit_cast(u32x2, v);
+        cs[m] = sq2(w2.y, sq2(w2.x, cs[m]));
+      }
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) colsum[256 * wave + c4 + q] = cs[q];
+    for (int m = 0; m < 4; ++m) colsum[256 * wave + 16 * (4 * m + g4) + jq16] = cs[m];
     __syncthreads();
     const float csum = (colsum[t] + colsum[256 + t]) + (colsum[512 + t] + colsum[768 + t]);
+    const float rsum = (rowpart[t] + rowpart[256 + t]) + (rowpart[512 + t] + rowpart[768 + t]);
     g.rpart[mat * g.stride_rpart + static_cast<int64_t>(tj) * (g.tiles_m * 256) + rowA0 + t] = rsum;
     g.cpart[mat * g.stride_cpart + static_cast<int64_t>(ti) * g.ldc + rowB0 + t] = csum;
   }
