@@ -23,6 +23,10 @@
 // conflicts.  The epilogue stages the output tile (and, for P, the A tile it adds) in
 // LDS and writes whole rows with 16-byte stores.  Same-shape matrices form one
 // launch; workgroup ids are remapped so each XCD receives a contiguous run of tiles.
+// Diagonal tiles of X X^T and of the polynomial's A A (a matrix times its own transpose) take
+// a path of their own that computes only the 36 needed 32 x 32 blocks from one operand.
+// Every lambda is forced inline: one left outlined would pass the accumulators by reference,
+// that is through scratch memory.
 #include <type_traits>
 
 #include "meq_internal.h"
@@ -120,6 +124,24 @@ __device__ __forceinline__ void sched_step() {
 #endif
 }
 
+
+// Scheduling pattern of one k step of a diagonal tile: nM MFMAs with the nR LDS reads of the next
+// step placed at the start, two after each of the first MFMAs (each step's fragment registers are
+// free once the previous step's MFMAs are issued), and the nD LDS-bound loads spread over the step.
+template <int nM, int nR, int nD, int m = 0>
+__device__ __forceinline__ void dsched() {
+#ifndef MEQ_NO_SCHED
+  if constexpr (m < nM) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    constexpr int r = (2 * m + 2 <= nR) ? 2 : (2 * m < nR ? nR - 2 * m : 0);  // two per MFMA, from the first
+    if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);
+    constexpr int d = (nD * (m + 2)) / nM - (nD * (m + 1)) / nM;
+    if constexpr (d > 0) __builtin_amdgcn_sched_group_barrier(0x020, d, 0);
+    dsched<nM, nR, nD, m + 1>();
+  }
+#endif
+}
+
 template <int kMode, bool kF16>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_ns_gemm(GemmArgs args) {
   constexpr bool kNN = kMode == 2;
@@ -209,7 +231,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int vB_nn0 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * (nn_r & 3))));
   const int vB_nn1 = 2 * (nn_r * ldb + rowB0 + 8 * ((lane & 31) ^ (4 * ((2 + nn_r) & 3))));
 
-  auto issue_half_a = [&](lds_u8* abuf, int kt, int i0 = 0, int i1 = kDma / 2) {
+  auto issue_half_a = [&](lds_u8* abuf, int kt, int i0 = 0, int i1 = kDma / 2) __attribute__((always_inline)) {
     const int k0 = kt * BK;
 #pragma unroll
     for (int i = i0; i < i1; ++i) {
@@ -217,7 +239,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       dma16(rA, abuf + I * 1024, (i & 1) ? vA_odd : vA, 2 * (kRowsPerDma * I * lda + k0));
     }
   };
-  auto issue_half_b = [&](lds_u8* bbuf, int kt, int i0 = 0, int i1 = kDma / 2) {
+  auto issue_half_b = [&](lds_u8* bbuf, int kt, int i0 = 0, int i1 = kDma / 2) __attribute__((always_inline)) {
     const int k0 = kt * BK;
 #pragma unroll
     for (int i = i0; i < i1; ++i) {
@@ -256,6 +278,243 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     nn_off[j] = nn_k * 512 + 16 * ((n >> 3) ^ nn_swz) + 2 * (n & 7);
   }
 
+  // Stage E (the polynomial's A tile, the same rows and columns as OUT, which starts at row
+  // out_row0 and column out_col0 of the matrix) in st0..st3: 32 instructions per stage, 2 rows each.
+  auto stage_e = [&](int out_row0, int out_col0) __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t rE = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(g.e + mat * g.stride_e), 0, 0x7fffffff, kBufferFlags);
+    const int lde = g.lde;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      lds_u8* dst = stage_of(q);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int I = 8 * wave + i;  // rows 2I, 2I + 1 of this stage
+        const int r = 64 * q + 2 * I + h;
+        const int c = (lane & 31) ^ (r & 31);
+        dma16(rE, dst + I * 1024, 2 * ((out_row0 + 64 * q + h) * lde + out_col0 + 8 * c), 2 * (2 * I * lde));
+      }
+    }
+    wait_vm<0>();
+    __syncthreads();
+  };
+
+  // Diagonal tile of a product of a matrix with itself (X X^T, A A): OUT is symmetric, and only the
+  // lower block triangle of OUT (36 of its 64 32 x 32 blocks, the product's upper triangle) is
+  // computed.  Waves 0 and 1 take the lower triangles of the two diagonal 128 x 128 quadrants (10
+  // blocks each, from the 4 fragments of their own rows, which serve both factors); waves 2 and 3
+  // take the two 128 x 64 halves of the off-diagonal quadrant (8 blocks each, from 2 + 4
+  // fragments).  Only operand A is fetched (the same 256 rows are both factors), into a ring of
+  // four 32 KiB buffers, three slabs ahead.
+  const bool dfast = kSym && ti == tj && g.a == g.b && g.lda == g.ldb && g.stride_a == g.stride_b;
+  if (dfast) {
+    if constexpr (kSym) {
+      const int nkd = g.K / BK;  // a multiple of 4
+      const bool roleD = wave < 2;
+      const int q = wave & 1;
+      auto dbar = []() __attribute__((always_inline)) {
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+      };
+      auto dmfma = [&](const bf16x8& x, const bf16x8& y, floatx16& c) __attribute__((always_inline)) {
+        if constexpr (kF16)
+          c = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(half8, x), __builtin_bit_cast(half8, y), c, 0, 0, 0);
+        else
+          c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, c, 0, 0, 0);
+      };
+      floatx16 dacc[10];
+#pragma unroll
+      for (int n = 0; n < 10; ++n)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dacc[n][v] = 0.f;
+      // fragment bases: role D rows 128 q + 32 i; role O A-side rows 64 q + 32 i, B-side 128 + 32 j
+      const int offD = (128 * q + (lane & 31)) * kRowBytes;
+      const int offOA = (64 * q + (lane & 31)) * kRowBytes;
+      const int offOB = (128 + (lane & 31)) * kRowBytes;
+      // slab kt's buffer is st[kt % 4]; during slab kt the loads of slab kt + 3 go into the buffer
+      // slab kt - 1 used (free since slab kt - 1's barrier); at slab kt's barrier the loads of
+      // slabs kt + 2 and the first 6 of kt + 3 may still be in flight.
+      issue_half_a(st0, 0);
+      issue_half_a(st1, 1);
+      issue_half_a(st2, 2);
+      wait_vm<16>();
+      dbar();
+      if (roleD) {
+        bf16x8 f[4], gq[4];
+        auto rd = [&](const lds_u8* buf, int kk, bf16x8 (&x)[4]) __attribute__((always_inline)) {
+          const int o = offD + slot_kk[kk];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) x[i] = *reinterpret_cast<const lds_bf16x8*>(buf + o + i * 32 * kRowBytes);
+        };
+        auto mf = [&](const bf16x8 (&x)[4]) __attribute__((always_inline)) {
+          int n = 0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = i; j < 4; ++j) dmfma(x[i], x[j], dacc[n++]);
+        };
+        auto dslab = [&](const lds_u8* cur, const lds_u8* nxt, lds_u8* fr, int kt) __attribute__((always_inline)) {
+          const int kl = min(kt + 3, nkd - 1);
+          rd(cur, 1, gq);
+          issue_half_a(fr, kl, 0, 2);
+          mf(f);
+          dsched<10, 4, 2>();
+          rd(cur, 2, f);
+          issue_half_a(fr, kl, 2, 4);
+          mf(gq);
+          dsched<10, 4, 2>();
+          rd(cur, 3, gq);
+          issue_half_a(fr, kl, 4, 6);
+          mf(f);
+          dsched<10, 4, 2>();
+          __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+          wait_vm<14>();
+          dbar();
+          issue_half_a(fr, kl, 6, 8);
+          rd(nxt, 0, f);
+          mf(gq);
+          dsched<10, 4, 2>();
+        };
+        rd(st0, 0, f);
+        for (int kt = 0; kt < nkd; kt += 4) {
+          dslab(st0, st1, st3, kt);
+          dslab(st1, st2, st0, kt + 1);
+          dslab(st2, st3, st1, kt + 2);
+          dslab(st3, st0, st2, kt + 3);
+        }
+      } else {
+        bf16x8 fa[2], fb[4], ga[2], gb[4];
+        auto rd = [&](const lds_u8* buf, int kk, bf16x8 (&xa)[2], bf16x8 (&xb)[4]) __attribute__((always_inline)) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            xa[i] = *reinterpret_cast<const lds_bf16x8*>(buf + offOA + slot_kk[kk] + i * 32 * kRowBytes);
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            xb[j] = *reinterpret_cast<const lds_bf16x8*>(buf + offOB + slot_kk[kk] + j * 32 * kRowBytes);
+        };
+        auto mf = [&](const bf16x8 (&xa)[2], const bf16x8 (&xb)[4]) __attribute__((always_inline)) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) dmfma(xa[i], xb[j], dacc[4 * i + j]);
+        };
+        auto dslab = [&](const lds_u8* cur, const lds_u8* nxt, lds_u8* fr, int kt) __attribute__((always_inline)) {
+          const int kl = min(kt + 3, nkd - 1);
+          rd(cur, 1, ga, gb);
+          issue_half_a(fr, kl, 0, 2);
+          mf(fa, fb);
+          dsched<8, 6, 2>();
+          rd(cur, 2, fa, fb);
+          issue_half_a(fr, kl, 2, 4);
+          mf(ga, gb);
+          dsched<8, 6, 2>();
+          rd(cur, 3, ga, gb);
+          issue_half_a(fr, kl, 4, 6);
+          mf(fa, fb);
+          dsched<8, 6, 2>();
+          __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+          wait_vm<14>();
+          dbar();
+          issue_half_a(fr, kl, 6, 8);
+          rd(nxt, 0, fa, fb);
+          mf(ga, gb);
+          dsched<8, 6, 2>();
+        };
+        rd(st0, 0, fa, fb);
+        for (int kt = 0; kt < nkd; kt += 4) {
+          dslab(st0, st1, st3, kt);
+          dslab(st1, st2, st0, kt + 1);
+          dslab(st2, st3, st1, kt + 2);
+          dslab(st3, st0, st2, kt + 3);
+        }
+      }
+      wait_vm<0>();
+      __syncthreads();
+      const int out_row0 = rowB0, out_col0 = rowA0, ldo = g.ldc;
+      float s = 1.f;
+      if (g.scale_kind != 0) s = g.fold[2 * mat + (g.scale_kind - 1)];
+      const float ae = g.alpha_e * s, aa = g.alpha_acc * s, ad = g.alpha_diag * s;
+      if (kHasE) stage_e(out_row0, out_col0);
+      // block with A-side rows RA.. and B-side rows RB..: lane holds OUT[RB + lane%32][RA + 8 (v/4) + 4h + v%4]
+      // Off-diagonal 32 x 32 blocks are also written transposed (OUT[c][r] = OUT[r][c]) with 2-byte
+      // stores; the 8 diagonal 32 x 32 blocks keep both of their triangles as the matrix cores
+      // form them, as in the general path.
+      typedef __attribute__((address_space(3))) uint16_t lds_u16;
+      auto emit = [&](const floatx16& a, int RA, int RB, auto out16_tag) __attribute__((always_inline)) {
+        constexpr bool kOut16 = decltype(out16_tag)::value;
+        const int r = RB + (lane & 31);
+        lds_u8* dst = stage_of(r >> 6);
+        u32x2 e[4];
+        if (kHasE) {
+#pragma unroll
+          for (int vq = 0; vq < 4; ++vq)
+            e[vq] = *reinterpret_cast<const lds_u32x2*>(dst + stage_byte(r, RA + 8 * vq + 4 * h));
+        }
+#pragma unroll
+        for (int vq = 0; vq < 4; ++vq) {
+          const int c = RA + 8 * vq + 4 * h;
+          float o[4];
+#pragma unroll
+          for (int qq = 0; qq < 4; ++qq) o[qq] = aa * a[4 * vq + qq];
+          if (kHasE) {
+            auto up = [](uint32_t x) { return kF16 ? f16_to_f32(x) : bf16_to_f32(x); };
+            o[0] = fmaf(ae, up(e[vq].x & 0xffffu), o[0]);
+            o[1] = fmaf(ae, up(e[vq].x >> 16), o[1]);
+            o[2] = fmaf(ae, up(e[vq].y & 0xffffu), o[2]);
+            o[3] = fmaf(ae, up(e[vq].y >> 16), o[3]);
+          }
+#pragma unroll
+          for (int qq = 0; qq < 4; ++qq) o[qq] += (r == c + qq) ? ad : 0.f;
+          u32x2 pk;
+          pk.x = kOut16 ? pack_f16x2(o[0], o[1]) : pack_bf16x2(o[0], o[1]);
+          pk.y = kOut16 ? pack_f16x2(o[2], o[3]) : pack_bf16x2(o[2], o[3]);
+          *reinterpret_cast<lds_u32x2*>(dst + stage_byte(r, c)) = pk;
+          if (RA != RB) {
+            const uint32_t hv[4] = {pk.x & 0xffffu, pk.x >> 16, pk.y & 0xffffu, pk.y >> 16};
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq)
+              *reinterpret_cast<lds_u16*>(stage_of((c + qq) >> 6) + stage_byte(c + qq, r)) = static_cast<uint16_t>(hv[qq]);
+          }
+        }
+      };
+      auto emit_all = [&](auto out16_tag) __attribute__((always_inline)) {
+        if (roleD) {
+          int n = 0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = i; j < 4; ++j) emit(dacc[n++], 128 * q + 32 * i, 128 * q + 32 * j, out16_tag);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) emit(dacc[4 * i + j], 64 * q + 32 * i, 128 + 32 * j, out16_tag);
+        }
+      };
+      if (g.out_f16)
+        emit_all(std::true_type{});
+      else
+        emit_all(std::false_type{});
+      __syncthreads();
+      // whole-row stores of OUT, as for the other tiles
+      uint16_t* __restrict__ Cd = g.c + mat * g.stride_c;
+#pragma unroll
+      for (int qs = 0; qs < 4; ++qs) {
+        const lds_u8* src = stage_of(qs);
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+          const int idx = it * 256 + t;
+          const int rr = idx >> 5, p = idx & 31;
+          const u32x4 v = *reinterpret_cast<const lds_u32x4*>(src + rr * 512 + 16 * p);
+          const int r = 64 * qs + rr;
+          const int c = p ^ (r & 31);
+          *reinterpret_cast<u32x4*>(Cd + static_cast<int64_t>(out_row0 + r) * ldo + out_col0 + 8 * c) = v;
+        }
+      }
+    }
+    return;
+  }
   floatx16 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -264,7 +523,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  auto load_frags = [&](const lds_u8* abuf, const lds_u8* bbuf, int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[4]) {
+  auto load_frags = [&](const lds_u8* abuf, const lds_u8* bbuf, int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[4]) __attribute__((always_inline)) {
     const int oa = offA + slot_kk[kk];
 #pragma unroll
     for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const lds_bf16x8*>(abuf + oa + i * 32 * kRowBytes);
@@ -284,7 +543,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
   };
 
-  auto mfma16 = [&](const bf16x8 (&af)[4], const bf16x8 (&bfr)[4]) {
+  auto mfma16 = [&](const bf16x8 (&af)[4], const bf16x8 (&bfr)[4]) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -317,7 +576,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // parts another 2-3%); operand B's extra slab of lead time is what makes that possible.
   const int nk = g.K / BK;
   bf16x8 fa[4], fb[4], ga[4], gb[4];
-  auto bar = [] {
+  auto bar = []() __attribute__((always_inline)) {
     // A bare barrier: __syncthreads() would also wait for the newer slabs' loads.  The
     // empty asm statements keep the compiler from moving memory accesses across it.
     asm volatile("" ::: "memory");
@@ -328,7 +587,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // ac, an: A buffers of slabs kt, kt + 1; bc, bn: B buffers of slabs kt, kt + 1; bp: the
   // B buffer of slab kt - 1, which receives slab kt + 2.  Past the end the loads are harmless
   // reloads of the last slab.
-  auto slab = [&](lds_u8* ac, lds_u8* an, const lds_u8* bc, const lds_u8* bn, lds_u8* bp, int kt) {
+  auto slab = [&](lds_u8* ac, lds_u8* an, const lds_u8* bc, const lds_u8* bn, lds_u8* bp, int kt) __attribute__((always_inline)) {
     load_frags(ac, bc, 1, ga, gb);
     issue_half_a(an, min(kt + 1, nk - 1), 4, 8);  // second half of A of slab kt + 1
     mfma16(fa, fb);
@@ -380,7 +639,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
   wait_vm<0>();
   __syncthreads();
-
   // ---- epilogue.  OUT is the 256 x 256 tile written with whole-row stores:
   //   apply:     OUT = C(ti, tj); lane holds OUT[128 wm + 32 i + lane%32][128 wn + 32 j + 8 (v/4) + 4 (lane/32) + v%4]
   //   Gram/poly: OUT = C(tj, ti) = C(ti, tj)^T; lane holds OUT[128 wn + 32 j + lane%32][128 wm + 32 i + ...]
@@ -395,32 +653,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int own_col = kNN ? wn : wm;  // 128-column half holding this wave's OUT columns
   const int ldo = g.ldc;
 
-  if (kHasE) {
-    // stage E (the same rows and columns as OUT): 32 instructions per stage, 2 rows each
-    const __amdgpu_buffer_rsrc_t rE = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(g.e + mat * g.stride_e), 0, 0x7fffffff, kBufferFlags);
-    const int lde = g.lde;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      lds_u8* dst = stage_of(q);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int I = 8 * wave + i;  // rows 2I, 2I + 1 of this stage
-        const int r = 64 * q + 2 * I + h;
-        const int c = (lane & 31) ^ (r & 31);
-        dma16(rE, dst + I * 1024, 2 * ((out_row0 + 64 * q + h) * lde + out_col0 + 8 * c), 2 * (2 * I * lde));
-      }
-    }
-    wait_vm<0>();
-    __syncthreads();
-  }
+  if (kHasE) stage_e(out_row0, out_col0);
 
   // combine: each lane owns 4 consecutive OUT columns per (i, j, v/4).  Block by block
   // (fenced against the scheduler, which otherwise hoists every product at once and runs out
   // of registers), with the staged E values of the next block read while this one is
   // computed.  All staged E reads come before any staged write.
   u32x2 packed[4][4][4];
-  auto e_read = [&](int i, int j, u32x2 (&e)[4]) {
+  auto e_read = [&](int i, int j, u32x2 (&e)[4]) __attribute__((always_inline)) {
     const int r = 128 * own_row + 32 * (kNN ? i : j) + (lane & 31);
     const lds_u8* src = stage_of(2 * own_row + ((kNN ? i : j) >> 1));
 #pragma unroll
@@ -430,7 +670,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
   };
   // The output format is uniform over the workgroup: one copy of the loop per format.
-  auto combine = [&](auto out16_tag) {
+  auto combine = [&](auto out16_tag) __attribute__((always_inline)) {
     constexpr bool kOut16 = decltype(out16_tag)::value;
     u32x2 ecur[4], enext[4];
     if (kHasE) e_read(0, 0, ecur);
@@ -474,7 +714,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   else
     combine(std::false_type{});
   // x0^2 + x1^2 + acc for a packed bf16 pair (v_dot2: the bf16 products are exact in fp32)
-  auto sq2 = [](uint32_t x, float acc) {
+  auto sq2 = [](uint32_t x, float acc) __attribute__((always_inline)) {
     const bf16x2 v = __builtin_bit_cast(bf16x2, x);
     return __builtin_amdgcn_fdot2_f32_bf16(v, v, acc, false);
   };
