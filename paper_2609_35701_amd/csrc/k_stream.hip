@@ -128,47 +128,9 @@ __global__ __launch_bounds__(256) void k_momentum(MomentumArgs a) {
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   float ss = 0.f;
   uint16_t hv[8][4];  // tall: column q, rows 4 ty + k
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int row = r0 + (tall ? 4 * ty + k : ty + 16 * k);
-    const int col = c0 + 8 * tx;
-    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    if (row < m && col < n) {
-      const int64_t off = static_cast<int64_t>(row) * n + col;
-      if (!bp) {
-        if (vec) {
-          load8<kGradBf16>(a.g[mi], off, v);
-        } else {
-#pragma unroll
-          for (int q = 0; q < 8; ++q)
-            if (col + q < n)
-              v[q] = kGradBf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.g[mi])[off + q])
-                               : static_cast<const float*>(a.g[mi])[off + q];
-        }
-      } else if (vec) {
-        float g[8], b[8];
-        load8<kGradBf16>(a.g[mi], off, g);
-        load8<false>(bp, off, b);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          b[q] = fmaf(mu, b[q], g[q]);
-          v[q] = a.nesterov ? fmaf(mu, b[q], g[q]) : b[q];
-        }
-        *reinterpret_cast<float4*>(bp + off) = make_float4(b[0], b[1], b[2], b[3]);
-        *reinterpret_cast<float4*>(bp + off + 4) = make_float4(b[4], b[5], b[6], b[7]);
-      } else {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          if (col + q < n) {
-            const float gq = kGradBf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.g[mi])[off + q])
-                                       : static_cast<const float*>(a.g[mi])[off + q];
-            const float bq = fmaf(mu, bp[off + q], gq);
-            bp[off + q] = bq;
-            v[q] = a.nesterov ? fmaf(mu, bq, gq) : bq;
-          }
-        }
-      }
-    }
+  // The end of one row: the sum of squares, bf16 V and its store (wide) or its place in the
+  // LDS transpose (tall).
+  auto finish = [&](int k, int row, int col, const float (&v)[8]) __attribute__((always_inline)) {
     uint16_t h[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
@@ -180,6 +142,76 @@ __global__ __launch_bounds__(256) void k_momentum(MomentumArgs a) {
     } else {
 #pragma unroll
       for (int q = 0; q < 8; ++q) hv[q][k] = h[q];
+    }
+  };
+  if (bp && vec && r0 + kEwRows <= m && c0 + kEwCols <= n) {
+    // Interior tile with a momentum buffer (almost every tile): the four rows' loads all go out
+    // before any arithmetic, four times the bytes in flight of the row-by-row loop below.
+    const int col = c0 + 8 * tx;
+    float gv[4][8], bv[4][8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int64_t off = static_cast<int64_t>(r0 + (tall ? 4 * ty + k : ty + 16 * k)) * n + col;
+      load8<kGradBf16>(a.g[mi], off, gv[k]);
+      load8<false>(bp, off, bv[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = r0 + (tall ? 4 * ty + k : ty + 16 * k);
+      const int64_t off = static_cast<int64_t>(row) * n + col;
+      float v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        bv[k][q] = fmaf(mu, bv[k][q], gv[k][q]);
+        v[q] = a.nesterov ? fmaf(mu, bv[k][q], gv[k][q]) : bv[k][q];
+      }
+      *reinterpret_cast<float4*>(bp + off) = make_float4(bv[k][0], bv[k][1], bv[k][2], bv[k][3]);
+      *reinterpret_cast<float4*>(bp + off + 4) = make_float4(bv[k][4], bv[k][5], bv[k][6], bv[k][7]);
+      finish(k, row, col, v);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = r0 + (tall ? 4 * ty + k : ty + 16 * k);
+      const int col = c0 + 8 * tx;
+      float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if (row < m && col < n) {
+        const int64_t off = static_cast<int64_t>(row) * n + col;
+        if (!bp) {
+          if (vec) {
+            load8<kGradBf16>(a.g[mi], off, v);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+              if (col + q < n)
+                v[q] = kGradBf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.g[mi])[off + q])
+                                 : static_cast<const float*>(a.g[mi])[off + q];
+          }
+        } else if (vec) {
+          float g[8], b[8];
+          load8<kGradBf16>(a.g[mi], off, g);
+          load8<false>(bp, off, b);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            b[q] = fmaf(mu, b[q], g[q]);
+            v[q] = a.nesterov ? fmaf(mu, b[q], g[q]) : b[q];
+          }
+          *reinterpret_cast<float4*>(bp + off) = make_float4(b[0], b[1], b[2], b[3]);
+          *reinterpret_cast<float4*>(bp + off + 4) = make_float4(b[4], b[5], b[6], b[7]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            if (col + q < n) {
+              const float gq = kGradBf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.g[mi])[off + q])
+                                         : static_cast<const float*>(a.g[mi])[off + q];
+              const float bq = fmaf(mu, bp[off + q], gq);
+              bp[off + q] = bq;
+              v[q] = a.nesterov ? fmaf(mu, bq, gq) : bq;
+            }
+          }
+        }
+      }
+      finish(k, row, col, v);
     }
   }
   if (tall) {
@@ -392,6 +424,46 @@ __global__ __launch_bounds__(256) void k_update(UpdateArgs a) {
       for (int q = 0; q < 8; ++q) cs[q] = (col + q < n) ? scale[col + q] : 0.f;
     }
   }
+  // Unpacked U of own row 4 ty + k (tall) from the transposed chunks.
+  auto tall_u = [&](int k, float (&uu)[8]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const uint32_t w = (k < 2) ? tch[q].x : tch[q].y;
+      uu[q] = bf16_to_f32(static_cast<uint16_t>((k & 1) ? (w >> 16) : (w & 0xffffu)));
+    }
+  };
+  if (vec && r0 + kEwRows <= m && c0 + kEwCols <= n) {
+    // Interior tile (almost every tile): the four rows' loads of U, W and the row scales all go
+    // out before any arithmetic.
+    float uu[4][8], wv[4][8], sr[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = r0 + (tall ? 4 * ty + k : ty + 16 * k);
+      if (!tall) load8<true, true>(u, static_cast<int64_t>(row) * ldu + col, uu[k]);
+      load8<kParamBf16, true>(a.w[mi], static_cast<int64_t>(row) * n + col, wv[k]);
+      if (dir == 0) sr[k] = scale[row];
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = r0 + (tall ? 4 * ty + k : ty + 16 * k);
+      const int64_t off = static_cast<int64_t>(row) * n + col;
+      if (tall) tall_u(k, uu[k]);
+      float w[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) w[q] = fmaf(decay, wv[k][q], -step * (uu[k][q] * (dir == 0 ? sr[k] : cs[q])));
+      if (kParamBf16) {
+        uint16_t h[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) h[q] = f32_to_bf16(w[q]);
+        st_nt(pack_bf16x8(h), reinterpret_cast<uint4*>(static_cast<uint16_t*>(a.w[mi]) + off));
+      } else {
+        float* wp = static_cast<float*>(a.w[mi]);
+        *reinterpret_cast<float4*>(wp + off) = make_float4(w[0], w[1], w[2], w[3]);
+        *reinterpret_cast<float4*>(wp + off + 4) = make_float4(w[4], w[5], w[6], w[7]);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int row = r0 + (tall ? 4 * ty + k : ty + 16 * k);
@@ -400,11 +472,7 @@ __global__ __launch_bounds__(256) void k_update(UpdateArgs a) {
     if (!tall) {
       load8<true, true>(u, static_cast<int64_t>(row) * ldu + col, uu);
     } else {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const uint32_t w = (k < 2) ? tch[q].x : tch[q].y;
-        uu[q] = bf16_to_f32(static_cast<uint16_t>((k & 1) ? (w >> 16) : (w & 0xffffu)));
-      }
+      tall_u(k, uu);
     }
     float s[8];
     if (dir == 0) {
