@@ -189,14 +189,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   int tile = logical - mat * g.tiles_per_mat;
   int ti, tj;
   if (kSym) {
-    ti = 0;
-    int rowlen = g.tiles_m;
-    while (tile >= rowlen) {
-      tile -= rowlen;
-      ++ti;
-      --rowlen;
+    // A matrix's T diagonal tiles come after its T (T - 1) / 2 others when they take the short
+    // path of a matrix times itself (the short tiles then fill the end of the launch), and
+    // first when they carry the symmetrizing pass of two different factors.
+    const int T = g.tiles_m, noff = T * (T - 1) / 2;
+    const bool self = g.a == g.b && g.lda == g.ldb && g.stride_a == g.stride_b;
+    const int dpos = self ? noff : 0;
+    if (tile >= dpos && tile < dpos + T) {
+      ti = tj = tile - dpos;
+    } else {
+      if (tile >= dpos + T) tile -= T;
+      ti = 0;  // off-diagonal tiles row by row
+      int rowlen = T - 1;
+      while (tile >= rowlen) {
+        tile -= rowlen;
+        ++ti;
+        --rowlen;
+      }
+      tj = ti + 1 + tile;
     }
-    tj = ti + tile;
   } else {
     constexpr int kGroup = 8;  // tile rows per group: tiles sharing a column panel run close in time
     const int per = kGroup * g.tiles_n;
