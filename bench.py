@@ -186,7 +186,7 @@ XCDS = 8
 
 def ns_launch_flops(wl) -> dict:
     """Per step, for each NS kernel instantiation over all shape groups: (algorithmic symmetric-aware
-    flops, flops the 256 x 256 tiles execute, padding and the lower half of diagonal tiles
+    flops, flops of the 256 x 256 tiles by count, padding and the lower half of diagonal tiles
     included), under the default schedule and coefficients: X X^T runs in k_ns_gemm<0, false>
     (bf16 X, fp16 output), the Gram-space products in k_ns_gemm<0, true> and every polynomial in
     k_ns_gemm<1, true> (fp16 A); k_ns_gemm<1, false> only runs for coefficients that fail the fp16
@@ -237,9 +237,11 @@ def summarize_mfma(run_dir: str, out: str, command: str, workload: str, note: st
         f"(divided by 8: cycles the kernel template was active); SQ_VALU_MFMA_BUSY_CYCLES summed over all {SIMDS} "
         f"SIMDs (divided by {SIMDS} and by the active cycles: fraction of the time a SIMD's matrix core was busy); "
         "SQ_INSTS_VALU_MFMA_MOPS_BF16 (SQ_INSTS_VALU_MFMA_MOPS_F16 for the fp16 instantiations) x 512 = flops "
-        "the matrix cores executed, against the flops the "
-        "256 x 256 tiles execute by count (padding and the lower half of diagonal tiles of the symmetric "
-        "products included) and the algorithmic symmetric-aware flops of the step's schedule. "
+        "the matrix cores executed, against the flops of the 256 x 256 tiles by count (padding and the "
+        "lower half of diagonal tiles of the symmetric products included) and the algorithmic "
+        "symmetric-aware flops of the step's schedule. Diagonal tiles of X X^T and of the polynomial's A A "
+        "(a matrix times its own transpose) run only the 36 of their 64 32 x 32 blocks on or below OUT's "
+        "diagonal, so those two instantiations execute about 0.90 of their tile flops. "
         "k_ns_gemm<0, false> runs X X^T, k_ns_gemm<0, true> the fp16 Gram-space products P A, P T, P Q, "
         "k_ns_gemm<1, *> the polynomial of one-step (bf16) and longer (fp16) segments, "
         "k_ns_gemm<2, false> the X products.\n\n",
