@@ -348,7 +348,20 @@ def extras_leg(params, wl, lr: float, steps: int, warmup: int) -> dict:
     out["capped_workspace_hidden"] = time_steps(capped, g_hidden, lr, steps, warmup, [meq.K_APPLY])
     out["capped_workspace_hidden"].update({"workspace_bytes": capped.plan.workspace_bytes,
                                            "passes": capped.plan.passes})
-    del capped, g_hidden
+    del capped
+    # the NS-CV trajectory (row and column CVs of X_0 .. X_20 of every hidden matrix, the printed
+    # iteration replayed step by step): one call, timed around the whole call
+    trace_upd = meq.HiddenWeightUpdate(params)
+    meq.ns_cv_trace(trace_upd, g_hidden, 2)  # warm-up
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    meq.ns_cv_trace(trace_upd, g_hidden, 20)
+    torch.cuda.synchronize()
+    out["ns_cv_trace_hidden"] = {"kmax": 20, "matrices": len(params),
+                                 "ms_per_call": (time.perf_counter() - t0) * 1e3,
+                                 "note": "20 printed Newton-Schulz steps with CVs after each, host copy of the "
+                                         "CVs included"}
+    del trace_upd, g_hidden
     torch.cuda.empty_cache()
     # remaining 2D parameters: the Llama token embedding and LM head (32000 x 2048, untied), bf16
     aux_p = [torch.randn(32000, 2048, device=dev).mul_(0.02).to(torch.bfloat16) for _ in range(2)]
