@@ -100,3 +100,16 @@ def write_back(w: np.ndarray, u: np.ndarray, scale: np.ndarray, lr: float, rho: 
     prod = (step * us).astype(np.float32)
     exact = decay.astype(np.float64) * np.asarray(w, np.float64) - prod.astype(np.float64)
     return exact.astype(np.float32)  # one rounding: the fused multiply-add
+
+
+def momentum(b: np.ndarray, g: np.ndarray, mu: float, nesterov: bool):
+    """The momentum kernel's float32 arithmetic: B <- fma(mu, B, G), and the orthogonalized input
+    V = fma(mu, B, G) with Nesterov (else V = B). A product of two float32 values is exact in
+    float64, so one rounding of the float64 sum models the fused multiply-add (up to the rare
+    double rounding). Returns (B, V) in float32."""
+    mu32 = np.float64(np.float32(mu))
+    b32 = (mu32 * np.asarray(b, np.float32).astype(np.float64) + np.asarray(g, np.float32)).astype(np.float32)
+    if not nesterov:
+        return b32, b32
+    v32 = (mu32 * b32.astype(np.float64) + np.asarray(g, np.float32)).astype(np.float32)
+    return b32, v32

@@ -99,6 +99,14 @@ def test_nesterov_flag():
     run_and_check(wl, [0, 1], steps=3, hp=meq.default_hparams(nesterov=1), label="nesterov")
 
 
+def test_nesterov_fp32_cancelling_entries():
+    """fp32 gradients with Nesterov, where G + mu B cancels almost exactly at a few entries of the
+    second step: the bf16 V still matches V formed from the GPU's own momentum within one ulp."""
+    wl = workloads.custom([(253, 2559)], "f32", seed=9107, name="nesterov-f32-cancel")
+    run_and_check(wl, [0], steps=2, hp=meq.default_hparams(nesterov=1, ns_gram_steps=1, ns_steps=1),
+                  label=wl.name)
+
+
 def test_extreme_imbalance_block():
     wl = workloads.custom([(512, 1376), (1376, 512)], "bf16", sigma=2.0, hot_row_frac=0.01, hot_row_gain=100.0,
                           name="extreme")
