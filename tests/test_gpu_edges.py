@@ -10,7 +10,9 @@
   last matrix of each shape group checked against the oracle at every step;
 - the Gram-space schedule on hard spectra (rank 8 plus noise, a geometric spectrum) of segmented
   shapes: finite, and no further from the printed iteration's fp64 result than the printed bf16
-  iteration itself (plus 0.01; tests/test_ns_emulation.py pins the same margin on the CPU).
+  iteration itself (plus 0.01; tests/test_ns_emulation.py pins the same margin on the CPU);
+- invariance to the gradient's scale: the iteration starts from V / ||V||_F (eq. "ns"), so
+  gradients multiplied by 2^k give bitwise the same weights, both schedules, both dtypes.
 """
 import math
 
@@ -204,3 +206,43 @@ def test_segmented_schedule_on_hard_spectra(shape):
             errs[gram] = relerr(u, ref)
         log(f"[case]   NS error: Gram-space schedule {errs[3]:.4g}, printed iteration {errs[1]:.4g}")
         assert errs[3] <= errs[1] + 0.01
+
+
+class _Plan:
+    """The attributes of a Run that check_matrix_step reads, for a plan built by hand."""
+
+    def __init__(self, wl, params, upd, hp):
+        self.wl, self.params, self.upd, self.hp = wl, params, upd, hp
+
+
+@pytest.mark.parametrize("dtype,nesterov", [("f32", 0), ("bf16", 0), ("bf16", 1)])
+def test_update_is_invariant_to_gradient_scale(dtype, nesterov):
+    """Five copies of one matrix in one plan, with gradients multiplied by 2^-24 .. 2^24: every
+    kernel step scales exactly by a power of two while its values stay in fp32's normal range (the
+    bf16 rounding of V, the fp32 tile sums of squares, 1/||V||^2 and 1/||V|| from a correctly
+    rounded square root, the folded prescale), so the weights, U and the statistics are bitwise
+    those of the unscaled copy, which is checked against the oracle; the momenta scale exactly."""
+    exps = [-24, -12, 0, 12, 24]
+    ref = exps.index(0)
+    hp = meq.default_hparams(nesterov=nesterov)
+    for shape in [(384, 1000), (700, 700)]:  # Gram-space segments (L >= 2S after padding) and printed steps
+        log(f"[case] gradient scale 2^{exps} {shape} {dtype} nesterov {nesterov}")
+        wl = workloads.custom([shape], dtype, seed=71, name="scale")
+        w0 = workloads.weight_init(wl, 0)
+        params = [to_dev(w0, dtype) for _ in exps]
+        upd = meq.HiddenWeightUpdate(params, hp)
+        plan = _Plan(wl, params, upd, hp)
+        for step in range(2):
+            g = workloads.grad_at_step(wl, 0, step)
+            w_before = to_np(params[ref])
+            b_before = to_np(upd.momenta[ref])
+            upd.step([to_dev(g * np.float32(2.0 ** k), dtype) for k in exps], LR)
+            torch.cuda.synchronize()
+            stats = upd.stats()
+            check_matrix_step(plan, ref, w_before, b_before, g.astype(np.float64), LR, stats,
+                              f"scale {shape} {dtype} step {step}")
+            for i, k in enumerate(exps):
+                assert torch.equal(params[i], params[ref]), f"{shape} 2^{k} step {step}: weights differ"
+                assert torch.equal(upd.view(i, meq.BUF_U), upd.view(ref, meq.BUF_U)), f"2^{k}: U differs"
+                assert torch.equal(upd.momenta[i], upd.momenta[ref] * 2.0 ** k), f"2^{k}: momentum"
+                assert (stats[0][i], stats[1][i], stats[2][i]) == (stats[0][ref], stats[1][ref], stats[2][ref])
