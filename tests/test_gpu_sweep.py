@@ -1,16 +1,23 @@
-"""Randomized parity cases through the C ABI: each case draws, from its own seed, one to three
-matrices of random shapes (multiples of 256 give or take 3, or any size up to 1300), the
-parameter dtype, Nesterov momentum, the Newton-Schulz step count (1-5) and the Gram-space segment
-length (1-3), and sometimes a few hot rows, then runs two steps of Algorithm "MeqMuon" with every
-stage checked against the oracle (tests/gpu_support.check_matrix_step). The cases cover schedules,
-shape groups and tile edges that the hand-picked tests do not combine.
+"""Randomized parity cases through the C ABI, each drawn from its own seed:
+
+- hidden weights: one to three matrices of random shapes (multiples of 256 give or take 3, or
+  any size up to 1300), the parameter dtype, Nesterov momentum, the Newton-Schulz step count
+  (1-5), the Gram-space segment length (1-3) and sometimes a few hot rows; two steps of Algorithm
+  "MeqMuon" with every stage checked against the oracle (tests/gpu_support.check_matrix_step);
+- capped plans: three to eight hidden matrices under a random workspace cap, bit for bit the
+  uncapped plan's parameters, momenta and statistics after two steps;
+- the two-sided normalization of eq. "aux" and the global RMS of eq. "vector": random shapes
+  and lengths, dtypes, Nesterov and misaligned parameters, against the oracle.
+
+The cases cover schedules, shape groups, passes and tile edges that the hand-picked tests do not
+combine.
 """
 import numpy as np
 import pytest
 import torch
 
 import workloads
-from gpu_support import Run, check_matrix_step, log
+from gpu_support import Run, check_matrix_step, log, to_dev
 from paper_2609_35701_amd import meq
 
 pytestmark = pytest.mark.gpu
@@ -48,3 +55,66 @@ def test_random_case(case):
         for k in range(len(shapes)):
             check_matrix_step(run, k, w_before[k], b_before[k], grads[k].astype(np.float64), LR, stats,
                               f"{label} step {step} matrix {k}")
+
+
+def _cap_for(shapes, dtype, hp, rng):
+    """A workspace cap that splits the plan into several passes (the smallest the planner accepts
+    that is at most a random fraction of the uncapped workspace)."""
+    full = meq.Plan(shapes, dtype, hparams=hp).workspace_bytes
+    cap = max(full // int(rng.integers(2, 7)), 1 << 20)
+    while cap < full:
+        try:
+            if meq.Plan(shapes, dtype, hparams=hp, max_workspace_bytes=cap).passes >= 2:
+                return cap
+        except meq.MeqError as e:
+            assert e.status == meq.MEQ_ERR_WORKSPACE
+        cap = cap * 3 // 2
+    return 0
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_random_capped_plan(case):
+    rng = np.random.default_rng(20261203 + case)
+    shapes = [(int(rng.integers(1, 1301)), int(rng.integers(1, 1301))) for _ in range(int(rng.integers(3, 9)))]
+    dtype = "bf16" if rng.random() < 0.7 else "f32"
+    hp = meq.default_hparams(nesterov=int(rng.random() < 0.3), ns_gram_steps=int(rng.integers(1, 4)))
+    cap = _cap_for(shapes, dtype, hp, rng)
+    log(f"[case] capped case {case}: {shapes} {dtype} cap {cap}")
+    assert cap > 0, "no cap gives two passes"
+    wl = workloads.custom(shapes, dtype, seed=int(rng.integers(0, 10000)), name=f"capsweep-{case}")
+    w0 = [to_dev(workloads.weight_init(wl, i), dtype) for i in range(wl.count)]
+    ref = meq.HiddenWeightUpdate([w.clone() for w in w0], hp)
+    capped = meq.HiddenWeightUpdate([w.clone() for w in w0], hp, max_workspace_bytes=cap)
+    assert capped.plan.passes >= 2
+    for step in range(2):
+        g = [to_dev(workloads.grad_at_step(wl, i, step), dtype) for i in range(wl.count)]
+        ref.step(g, LR)
+        capped.step(g, LR)
+    torch.cuda.synchronize()
+    for k in range(wl.count):
+        assert torch.equal(ref.params[k], capped.params[k]), f"case {case}: parameter {k}"
+        assert torch.equal(ref.momenta[k], capped.momenta[k]), f"case {case}: momentum {k}"
+    assert ref.stats() == capped.stats()
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_random_aux_case(case):
+    from test_gpu_kinds import run_aux
+
+    rng = np.random.default_rng(20261204 + case)
+    shape = (int(rng.integers(1, 3001)), int(rng.integers(1, 2049)))
+    dtype = "bf16" if rng.random() < 0.6 else "f32"
+    hp = meq.default_hparams(nesterov=int(rng.random() < 0.4))
+    run_aux(shape, dtype, steps=2, seed=int(rng.integers(0, 10000)), hp=hp, offset=int(rng.random() < 0.3),
+            sigma=float(rng.choice([0.5, 1.0, 2.0])))
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_random_vector_case(case):
+    from test_gpu_kinds import run_vec
+
+    rng = np.random.default_rng(20261205 + case)
+    lengths = [int(x) for x in rng.integers(1, 200001, size=int(rng.integers(1, 12)))]
+    dtype = "bf16" if rng.random() < 0.6 else "f32"
+    hp = meq.default_hparams(nesterov=int(rng.random() < 0.4))
+    run_vec(lengths, dtype, steps=2, seed=int(rng.integers(0, 10000)), hp=hp, offset=int(rng.random() < 0.3))
