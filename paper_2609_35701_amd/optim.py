@@ -9,7 +9,9 @@ all with the momentum of eq. "momentum" and the write-back of eq. "meqmuon-updat
 """
 from __future__ import annotations
 
-from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+from typing import Dict, Iterable, List, Optional, Tuple
+
+import torch
 
 from . import meq
 
@@ -21,8 +23,6 @@ def split_parameters(model) -> Tuple[list, list, list]:
     are listed once).  vectors: every parameter with one dimension.  hidden: the other 2D
     parameters.  Parameters with more than two dimensions are rejected: the update is defined
     for matrices and vectors."""
-    import torch
-
     aux_ids = set()
     for name, mod in model.named_modules():
         if isinstance(mod, torch.nn.Embedding) or name.split(".")[-1] == "lm_head":
@@ -43,59 +43,72 @@ def split_parameters(model) -> Tuple[list, list, list]:
     return hidden, aux, vectors
 
 
-class MeqMuon:
-    """One optimizer over the three parameter kinds.
+class MeqMuon(torch.optim.Optimizer):
+    """One optimizer over the three parameter kinds, with the ``torch.optim.Optimizer`` interface.
 
-    Parameters of one kind may mix bf16 and fp32; each (kind, dtype) pair gets its own plan,
-    momenta and workspace.  ``step(lr)`` reads ``p.grad`` of every parameter (same dtype and shape
-    as the parameter) and enqueues all updates on the current torch stream.  ``hidden_hparams``
-    overrides the hyperparameters of the hidden weights only (for instance Nesterov momentum, as
-    in the paper's experiments, or the Moonlight-Muon rule)."""
+    Each kind is one parameter group (``group["kind"]`` is ``meq.PARAM_HIDDEN``, ``PARAM_AUX`` or
+    ``PARAM_VECTOR``) whose ``lr`` is read at every step, so the learning-rate schedulers of
+    ``torch.optim.lr_scheduler`` drive it.  Parameters of one kind may mix bf16 and fp32; each
+    (kind, dtype) pair gets its own plan, momenta and workspace.  ``step()`` reads ``p.grad`` of
+    every parameter (same dtype and shape as the parameter) and enqueues all updates on the
+    current torch stream.  ``hidden_hparams`` overrides the hyperparameters of the hidden weights
+    only (for instance Nesterov momentum, as in the paper's experiments, or the Moonlight-Muon
+    rule)."""
 
     def __init__(self, hidden: Iterable = (), aux: Iterable = (), vectors: Iterable = (), lr: float = 0.02,
                  hparams: Optional[meq.HParams] = None, hidden_hparams: Optional[meq.HParams] = None):
-        self.lr = float(lr)
+        kinds = [(meq.PARAM_HIDDEN, list(hidden)), (meq.PARAM_AUX, list(aux)), (meq.PARAM_VECTOR, list(vectors))]
+        super().__init__([{"params": ps, "kind": kind} for kind, ps in kinds if ps], {"lr": float(lr)})
         base = hparams if hparams is not None else meq.default_hparams()
+        # (parameter group, plan) pairs, one plan per (kind, dtype)
         self.updates: List[Tuple[int, meq.ParamUpdate]] = []
-        for kind, params, hp in ((meq.PARAM_HIDDEN, hidden, hidden_hparams or base),
-                                 (meq.PARAM_AUX, aux, base), (meq.PARAM_VECTOR, vectors, base)):
+        self._group_of: List[int] = []
+        for gi, group in enumerate(self.param_groups):
+            kind = group["kind"]
+            hp = (hidden_hparams or base) if kind == meq.PARAM_HIDDEN else base
             by_dtype: Dict[object, list] = {}
-            for p in params:
+            for p in group["params"]:
                 by_dtype.setdefault(p.dtype, []).append(p)
             for _, ps in sorted(by_dtype.items(), key=lambda kv: str(kv[0])):
                 self.updates.append((kind, meq.ParamUpdate(ps, hp, kind=kind)))
+                self._group_of.append(gi)
 
     @classmethod
     def for_model(cls, model, **kw) -> "MeqMuon":
         hidden, aux, vectors = split_parameters(model)
         return cls(hidden, aux, vectors, **kw)
 
-    def step(self, lr: Optional[float] = None) -> None:
-        lr = self.lr if lr is None else float(lr)
-        for _, upd in self.updates:
+    @torch.no_grad()
+    def step(self, closure=None, lr: Optional[float] = None):
+        """One update of every parameter.  ``lr`` overrides the groups' learning rates for this
+        step only; ``closure`` (re-evaluating the loss) is called first, as in torch optimizers."""
+        loss = None
+        if closure is not None:
+            with torch.enable_grad():
+                loss = closure()
+        for gi, (_, upd) in zip(self._group_of, self.updates):
+            step_lr = float(lr) if lr is not None else float(self.param_groups[gi]["lr"])
             grads = []
             for p in upd.params:
                 if p.grad is None:
                     raise ValueError("every parameter needs a gradient (p.grad) for a MeqMuon step")
                 grads.append(p.grad if p.grad.is_contiguous() else p.grad.contiguous())
-            upd.step(grads, lr)
-
-    def zero_grad(self) -> None:
-        for _, upd in self.updates:
-            for p in upd.params:
-                p.grad = None
+            upd.step(grads, step_lr)
+        return loss
 
     def state_dict(self) -> dict:
-        """Momenta (fp32, one per parameter, in construction order per plan) and the learning rate."""
-        return {"lr": self.lr, "momenta": [[b.detach().clone() for b in upd.momenta] for _, upd in self.updates]}
+        """torch's optimizer state (the parameter groups and their learning rates) plus the fp32
+        momenta, one list per plan in construction order."""
+        state = super().state_dict()
+        state["momenta"] = [[b.detach().clone() for b in upd.momenta] for _, upd in self.updates]
+        return state
 
     def load_state_dict(self, state: dict) -> None:
         moms = state["momenta"]
-        if len(moms) != len(self.updates):
+        if len(moms) != len(self.updates) or any(len(ms) != len(upd.momenta) for (_, upd), ms in zip(self.updates, moms)):
             raise ValueError("state does not match this optimizer's plans")
-        for (_, upd), ms in zip(self.updates, moms):
-            if len(ms) != len(upd.momenta):
-                raise ValueError("state does not match this optimizer's plans")
-            for b, m in zip(upd.momenta, ms):
-                b.copy_(m)
-        self.lr = float(state.get("lr", self.lr))
+        super().load_state_dict({k: v for k, v in state.items() if k != "momenta"})
+        with torch.no_grad():
+            for (_, upd), ms in zip(self.updates, moms):
+                for b, m in zip(upd.momenta, ms):
+                    b.copy_(m)

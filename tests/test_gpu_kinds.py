@@ -336,3 +336,57 @@ def test_meqmuon_optimizer_trains_tiny_model_and_keeps_its_momenta():
         for p, b in zip(upd.params, upd.momenta):
             want = ref[id(p)]
             assert relerr(to_np(b).reshape(want.shape), want) <= 1e-5, f"momentum of {tuple(p.shape)}"
+
+
+def test_meqmuon_follows_an_lr_scheduler_and_resumes_from_its_state_dict():
+    """MeqMuon is a torch optimizer: a LambdaLR schedule sets each parameter group's rate (0 at the
+    first step, where every weight keeps its value, since the decay 1 - lr lambda is exactly 1, and
+    the momenta take the gradients), and a model and optimizer restored from state_dict() after
+    three steps continue bit for bit as the uninterrupted run (the same recorded gradients)."""
+    import copy
+
+    from paper_2609_35701_amd.optim import MeqMuon
+    from tiny_model import Tiny
+
+    torch.manual_seed(4)
+    model = Tiny().to("cuda:0").to(torch.bfloat16)
+    tok = torch.randint(0, 96, (4, 24), device="cuda:0")
+    ramp = lambda s: min(1.0, s / 2.0)  # noqa: E731  (0, 0.5, 1, 1, ...)
+    opt = MeqMuon.for_model(model, lr=0.02)
+    sch = torch.optim.lr_scheduler.LambdaLR(opt, ramp)
+    assert sorted(g["kind"] for g in opt.param_groups) == [meq.PARAM_HIDDEN, meq.PARAM_AUX, meq.PARAM_VECTOR]
+    w0 = [p.detach().clone() for p in model.parameters()]
+    recorded, snap = [], None
+    for step in range(6):
+        model.zero_grad(set_to_none=True)
+        loss = torch.nn.functional.cross_entropy(model(tok[:, :-1]).float().reshape(-1, 96), tok[:, 1:].reshape(-1))
+        loss.backward()
+        recorded.append([p.grad.detach().clone() for p in model.parameters()])
+        assert all(g["lr"] == 0.02 * ramp(step) for g in opt.param_groups)
+        opt.step()
+        sch.step()
+        if step == 0:
+            torch.cuda.synchronize()
+            assert all(torch.equal(p, q) for p, q in zip(model.parameters(), w0)), "lr 0 moved a weight"
+            for _, upd in opt.updates:
+                for p, b in zip(upd.params, upd.momenta):
+                    assert torch.equal(b, p.grad.float()), "first momentum is the gradient"
+        if step == 2:
+            snap = (copy.deepcopy(model.state_dict()), copy.deepcopy(opt.state_dict()), copy.deepcopy(sch.state_dict()))
+    model2 = Tiny().to("cuda:0").to(torch.bfloat16)
+    model2.load_state_dict(snap[0])
+    opt2 = MeqMuon.for_model(model2, lr=0.5)  # rates and momenta come from the state
+    sch2 = torch.optim.lr_scheduler.LambdaLR(opt2, ramp)
+    opt2.load_state_dict(snap[1])
+    sch2.load_state_dict(snap[2])
+    for step in range(3, 6):
+        for p, g in zip(model2.parameters(), recorded[step]):
+            p.grad = g.clone()
+        opt2.step()
+        sch2.step()
+    torch.cuda.synchronize()
+    for p, q in zip(model.parameters(), model2.parameters()):
+        assert torch.equal(p, q), f"resumed weight {tuple(p.shape)}"
+    for (_, u1), (_, u2) in zip(opt.updates, opt2.updates):
+        for b1, b2 in zip(u1.momenta, u2.momenta):
+            assert torch.equal(b1, b2), "resumed momentum"
