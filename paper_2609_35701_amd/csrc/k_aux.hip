@@ -170,19 +170,24 @@ __global__ __launch_bounds__(256) void k_aux_cols(AuxArgs a) {
   }
 }
 
-// 64 columns per block; the four waves take every fourth row block and meet in LDS,
-// added in a fixed order.
+// 16 columns per block: the 16 threads of a column each sum every 16th row block (short
+// chains of loads, and enough blocks to spread over the CUs), then meet in LDS, added in a
+// fixed order.
 __global__ __launch_bounds__(256) void k_aux_colfin(AuxArgs a) {
-  __shared__ double part[4][64];
-  const int jj = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int j = blockIdx.x * 64 + jj;
+  __shared__ double part[16][16];
+  const int jj = threadIdx.x & 15, w = threadIdx.x >> 4;
+  const int j = blockIdx.x * 16 + jj;
   double t = 0.0;
   if (j < a.n)
-    for (int k = w; k < a.row_blocks; k += 4) t += a.cpart[static_cast<int64_t>(k) * a.n + j];
+    for (int k = w; k < a.row_blocks; k += 16) t += a.cpart[static_cast<int64_t>(k) * a.n + j];
   part[w][jj] = t;
   __syncthreads();
   if (w == 0 && j < a.n) {
-    const double sum = (part[0][jj] + part[1][jj]) + (part[2][jj] + part[3][jj]);
+    double q4[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      q4[q] = (part[4 * q][jj] + part[4 * q + 1][jj]) + (part[4 * q + 2][jj] + part[4 * q + 3][jj]);
+    const double sum = (q4[0] + q4[1]) + (q4[2] + q4[3]);
     const double c = sqrt(sum / a.m);
     a.crms[j] = c;
     a.cscale[j] = c > a.delta ? static_cast<float>(1.0 / c) : 0.f;
@@ -325,7 +330,7 @@ hipError_t launch_aux_cols(const AuxArgs& a, int grad_bf16, hipStream_t st) {
 }
 
 hipError_t launch_aux_colfin(const AuxArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_aux_colfin, dim3((a.n + 63) / 64), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(k_aux_colfin, dim3((a.n + 15) / 16), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
