@@ -77,3 +77,43 @@ def test_step_captured_in_a_graph_replays_like_eager():
             for j, (b, c) in enumerate(zip(ups[name].momenta, bs)):
                 assert torch.equal(b, c), f"replay {k}: {name} momentum {j} differs from the eager step"
     graph.reset()
+
+
+def test_meqmuon_step_captured_in_a_graph_replays_like_eager():
+    """MeqMuon.step() over a whole model whose gradients live in fixed tensors is captured once and
+    replayed; after every replay the weights and momenta equal those of an eager optimizer given
+    the same gradients (the learning rate is the one the groups held at capture)."""
+    import copy
+
+    from paper_2609_35701_amd.optim import MeqMuon
+    from tiny_model import Tiny
+
+    dev = torch.device("cuda:0")
+    torch.manual_seed(5)
+    m_eager = Tiny().to(dev).to(torch.bfloat16)
+    m_graph = copy.deepcopy(m_eager)
+    grads = [[_seeded(tuple(p.shape), 100 * k + i, 1e-3, p.dtype, dev) for i, p in enumerate(m_eager.parameters())]
+             for k in range(3)]
+    opt_eager = MeqMuon.for_model(m_eager, lr=0.02)
+    opt_graph = MeqMuon.for_model(m_graph, lr=0.02)
+    for p in m_graph.parameters():
+        p.grad = torch.zeros_like(p)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        opt_graph.step()
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(m_eager.parameters(), m_graph.parameters())), "capture ran a step"
+    for k in range(3):
+        for p, g in zip(m_eager.parameters(), grads[k]):
+            p.grad = g.clone()
+        opt_eager.step()
+        for p, g in zip(m_graph.parameters(), grads[k]):
+            p.grad.copy_(g)
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(m_eager.parameters(), m_graph.parameters()):
+            assert torch.equal(a, b), f"replay {k}: weight {tuple(a.shape)}"
+        for (_, ue), (_, ug) in zip(opt_eager.updates, opt_graph.updates):
+            for be, bg in zip(ue.momenta, ug.momenta):
+                assert torch.equal(be, bg), f"replay {k}: momentum"
