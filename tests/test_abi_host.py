@@ -402,3 +402,52 @@ def test_step_static_rejects_plans_beyond_its_scratch_before_any_device_work():
     capped = meq.Plan([(m.rows, m.cols) for m in workloads.workload("llama-1b").matrices], "bf16",
                       max_workspace_bytes=meq.MEQ_STATIC_SCRATCH_BYTES)
     assert capped.workspace_bytes <= meq.MEQ_STATIC_SCRATCH_BYTES
+
+
+C_PROGRAM = r"""
+#include <stdio.h>
+#include "meq.h"
+
+/* plain C against the C ABI: plan the 1B shapes (one of each, tall included) on the host */
+int main(void) {
+  meq_hparams hp;
+  meq_default_hparams(&hp);
+  const meq_matrix_desc mats[4] = {{2048, 2048, MEQ_BF16, MEQ_BF16}, {512, 2048, MEQ_BF16, MEQ_BF16},
+                                   {2048, 8192, MEQ_BF16, MEQ_BF16}, {8192, 2048, MEQ_BF16, MEQ_BF16}};
+  meq_plan* plan = NULL;
+  meq_status st = meq_init(mats, 4, &hp, &plan);
+  if (st != MEQ_OK) {
+    printf("init %d %s\n", (int)st, meq_status_string(st));
+    return 1;
+  }
+  printf("steps %d gram %d groups %d ws %zu\n", (int)hp.ns_steps, (int)hp.ns_gram_steps,
+         (int)meq_plan_num_groups(plan), meq_workspace_bytes(plan));
+  meq_destroy(plan);
+  st = meq_init(mats, 4, &hp, NULL);
+  printf("null %s\n", meq_status_string(st));
+  return 0;
+}
+"""
+
+
+def test_header_compiles_and_links_as_c(tmp_path):
+    """The header is plain C: a C11 program built with gcc against include/meq.h and linked with the
+    built library plans the 1B shapes on the host, and agrees with the Python binding."""
+    import shutil
+    import subprocess
+
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use_meq.c"
+    src.write_text(C_PROGRAM)
+    exe = tmp_path / "use_meq"
+    libdir = os.path.dirname(meq.LIB_PATH)
+    cmd = [gcc, "-std=c11", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+           "-I" + os.path.join(ROOT, "include"), str(src), "-L" + libdir, "-lmeq", "-Wl,-rpath," + libdir,
+           "-o", str(exe)]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True, timeout=60).stdout.split("\n")
+    plan = meq.Plan([(2048, 2048), (512, 2048), (2048, 8192), (8192, 2048)], "bf16")
+    assert out[0] == f"steps 5 gram 3 groups {len(plan.groups())} ws {plan.workspace_bytes}", out[0]
+    assert out[1] == "null " + meq.status_string(meq.MEQ_ERR_INVALID_ARG), out[1]
